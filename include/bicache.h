@@ -1,0 +1,237 @@
+/*
+ * bicache.h -- C ABI of libbicache.so: BiCache's shared-prefix denoising step
+ * for diffusion language models on AMD Instinct MI355X (gfx950).
+ *
+ * The method (BiCache, "bidirectional prefix caching"):
+ *   - A shared prefix p is run once on its own ("populate", Sec. 5.2: on a
+ *     miss the KVs of p are computed at the first step for all layers and
+ *     stored in the KV store H under the key h(p)).
+ *   - A denoising step of a batch of requests that share p runs the layers
+ *     shallower than the reuse depth d on the suffix rows only, attending over
+ *     the cached prefix K/V plus the request's own suffix K/V (Eq. 4), and
+ *     recomputes the prefix in the layers at or beyond d with full
+ *     bidirectional attention (refresh case of Eq. 5).  The paper's depth b
+ *     (1-based, layers l <= b reuse the cache) is d here (0-based, l < d).
+ *
+ * Conventions for every entry point:
+ *   - Device buffers are allocated and owned by the caller.  The library never
+ *     allocates or frees device memory; it keeps host-side metadata only.
+ *   - Tensors are dense, row-major, bf16 = IEEE bfloat16 bits (uint16), fp32 =
+ *     IEEE binary32.  Device pointers must be 16-byte aligned.
+ *   - `stream` is a hipStream_t passed as an opaque pointer (NULL = the null
+ *     stream).  Every device operation is enqueued asynchronously on it; no
+ *     call synchronizes the host.
+ *   - No C++ exception crosses this boundary.  Every call returns a bc_status;
+ *     bc_last_error() gives a message for the calling thread's last failure.
+ *     All arguments are validated before anything is enqueued, so a call that
+ *     returns BC_E_INVALID / BC_E_NOT_FOUND / BC_E_STATE has no side effect.
+ *   - A bc_model is not thread-safe: calls on one model must not overlap.
+ *
+ * The layer is a pre-norm transformer block: RMSNorm, fused Q/K/V projection
+ * (Eq. 1), rotate-half RoPE, unmasked attention (Eq. 2), output projection
+ * plus residual, RMSNorm, SwiGLU FFN plus residual, no biases.  The residual
+ * stream is fp32; GEMM and attention operands are bf16 with fp32
+ * accumulation.
+ */
+#ifndef BICACHE_H
+#define BICACHE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+  BC_OK = 0,
+  BC_E_INVALID = -1,   /* bad argument: null pointer, size, range or shape */
+  BC_E_NOT_FOUND = -2, /* step/lookup on a key that is not cached (the paper's miss) */
+  BC_E_OOM = -3,       /* host allocation failed */
+  BC_E_HIP = -4,       /* a HIP runtime call failed (includes earlier async faults) */
+  BC_E_STATE = -5,     /* operation not allowed in this state (e.g. key already cached) */
+  BC_E_CAPACITY = -6   /* a size is beyond what a kernel supports */
+} bc_status;
+
+/* Message of the calling thread's last failed call ("" if none).  The pointer
+ * stays valid until the next call on the same thread. */
+const char* bc_last_error(void);
+
+/* ------------------------------------------------------------------ model */
+
+typedef struct {
+  int n_layers;    /* L >= 1 */
+  int hidden;      /* h, multiple of 64 */
+  int n_heads;     /* Hq query heads */
+  int n_kv_heads;  /* Hkv KV heads, Hq % Hkv == 0 (grouped-query attention:
+                      query head j reads KV head j / (Hq/Hkv)) */
+  int head_dim;    /* dh: 64 or 128 */
+  int ffn;         /* F, SwiGLU width, multiple of 64 */
+  float rms_eps;   /* RMSNorm epsilon */
+  float rope_theta;/* RoPE base; pair (i, i+dh/2) rotates by pos*theta^(-2i/dh) */
+} bc_model_config;
+
+/* Device pointers to one layer's weights, all bf16, [out, in] row-major.
+ * w_qkv     [(Hq + 2*Hkv)*dh, h]: rows of the Hq query heads, then the Hkv key
+ *           heads, then the Hkv value heads, each head's dh rows contiguous.
+ * w_o       [h, Hq*dh]
+ * w_gate_up [2*F, h]: rows 0..F-1 gate, rows F..2F-1 up;
+ *           ffn(x) = w_down (silu(gate x) * (up x)).
+ * w_down    [h, F]
+ * attn_norm, ffn_norm [h]: RMSNorm gains.
+ * The weights are referenced, not copied, and must outlive the model. */
+typedef struct {
+  const void* w_qkv;
+  const void* w_o;
+  const void* w_gate_up;
+  const void* w_down;
+  const void* attn_norm;
+  const void* ffn_norm;
+} bc_layer_weights;
+
+typedef struct bc_model bc_model;
+
+/* Creates a model over caller-owned weights (`layers` has cfg->n_layers
+ * entries; the array itself is copied).  cache_capacity >= 1 is the number of
+ * prefixes the KV store H holds before FIFO eviction (Appendix C).  Host only:
+ * enqueues nothing. */
+bc_status bc_model_create(const bc_model_config* cfg, const bc_layer_weights* layers,
+                          int cache_capacity, bc_model** out);
+/* Destroys the model and its table.  Cache memory stays the caller's. */
+bc_status bc_model_destroy(bc_model* model);
+
+/* --------------------------------------------------------- prefix cache */
+
+/* Device bytes of one cache entry for a prefix of m tokens caching the first
+ * n_layers_to_cache (Lc) layers, 0 <= Lc <= L.  Layout (byte offsets from the
+ * entry base, see bc_cache_offset):
+ *   KV$  [Lc][2 (K, V)][Hkv][m][dh] bf16, post-RoPE prefix keys and values of
+ *        the prefix-only forward (KV$_l of Eq. 4);
+ *   H$   at the next 256-byte boundary: [min(Lc+1, L)][m][h] fp32, the prefix
+ *        residual entering layers 0..min(Lc, L-1) (H$[0] is the input itself).
+ * Returns 0 for invalid arguments. */
+size_t bc_prefix_cache_bytes(const bc_model* model, int m, int n_layers_to_cache);
+
+/* Byte offset inside such an entry of element (layer, part, head, pos, dim):
+ * part 0 = K, 1 = V (head < Hkv, dim < dh, layer < Lc), 2 = H$ (head ignored,
+ * dim < h, layer <= min(Lc, L-1)).  Returns (size_t)-1 when out of range. */
+size_t bc_cache_offset(const bc_model* model, int m, int n_layers_to_cache, int layer, int part,
+                       int head, int pos, int dim);
+
+/* Device workspace bytes that bc_prefix_populate needs for a prefix of m tokens. */
+size_t bc_populate_workspace_bytes(const bc_model* model, int m);
+
+/* Populate on a miss (Sec. 5.2): runs the prefix-only forward x_pref = p at
+ * positions 0..m-1 through layers 0..Lc-1, writes the entry into cache_mem
+ * (layout above) and inserts `key` into the store.  If the store is full the
+ * oldest entry is evicted first: *evicted = 1 and *evicted_key = its key (the
+ * caller may free that entry's memory once `stream` has passed this call);
+ * otherwise *evicted = 0, *evicted_key = 0 (either output may be NULL).
+ *   x_prefix   device bf16 [m, h], m >= 1
+ *   cache_mem  device, >= bc_prefix_cache_bytes(model, m, Lc) bytes, 256-byte
+ *              aligned, referenced by the entry until it is invalidated or
+ *              evicted
+ *   workspace  device, >= bc_populate_workspace_bytes(model, m) bytes, free for
+ *              reuse once `stream` has passed this call
+ * Errors: BC_E_STATE if `key` is already cached (invalidate it first),
+ * BC_E_INVALID for bad sizes or pointers, BC_E_HIP if a launch fails (the key
+ * is then not inserted). */
+bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix, int m,
+                             int n_layers_to_cache, void* cache_mem, size_t cache_bytes,
+                             void* workspace, size_t ws_bytes, void* stream,
+                             uint64_t* evicted_key, int* evicted);
+
+/* Looks up `key` in the store (the paper's O(1) hit test).  On a hit writes the
+ * entry's m and Lc (either pointer may be NULL) and returns BC_OK; on a miss
+ * returns BC_E_NOT_FOUND. */
+bc_status bc_prefix_lookup(const bc_model* model, uint64_t key, int* m_out, int* n_layers_out);
+
+/* Removes `key` from the store (BC_E_NOT_FOUND if absent).  The entry's memory
+ * returns to the caller once work already enqueued on it has completed. */
+bc_status bc_prefix_invalidate(bc_model* model, uint64_t key);
+
+/* Writes up to max_keys cached keys, oldest first (the FIFO eviction order),
+ * and their total count to *n_out. */
+bc_status bc_cache_keys(const bc_model* model, uint64_t* keys, int max_keys, int* n_out);
+
+/* Prefix key k = h(p) of Appendix C: 64-bit xxHash (XXH64, seed 0) over the
+ * token IDs as little-endian int32.  Host only. */
+uint64_t bc_prefix_key(const int32_t* token_ids, size_t n);
+
+/* ------------------------------------------------------------------ step */
+
+/* Device workspace bytes that bc_step_forward needs. */
+size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int d);
+
+/* Work accounting of a step, host only, exactly what bc_step_forward launches:
+ * for each layer l (arrays of n_layers ints, any may be NULL)
+ *   rows[l]      token rows projected by layer l: B*n_s if l < d, B*(m+n_s) otherwise
+ *   pos_base[l]  RoPE position of the first projected row of a request:
+ *                m for l < d (suffix positions m..m+n_s-1), 0 otherwise
+ *   reads_kv[l]  1 if layer l reads the cached KV$_l (l < d), else 0
+ * and *reads_h (may be NULL) = the H$ layer re-entered at d (d < L), or -1. */
+bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int* rows,
+                       int* pos_base, int* reads_kv, int* reads_h);
+
+/* One denoising-step forward of B requests sharing the cached prefix `key`
+ * (Eq. 4 for layers l < d, the refresh case of Eq. 5 for l >= d).
+ *   x_suffix  device bf16 [B, n_s, h]: each request's non-shared rows z_t, at
+ *             positions m..m+n_s-1
+ *   d         reuse depth, 0 <= d <= L and d <= the entry's Lc; d = 0 is the
+ *             un-cached forward, d = L reuses the cache in every layer
+ *   out       device fp32 [B, n_s, h]: final residual of the suffix rows (no
+ *             final norm, no LM head)
+ *   workspace device, >= bc_step_workspace_bytes(model, m, B, n_s, d) bytes
+ * Requests never attend to each other.  Errors: BC_E_NOT_FOUND on a miss,
+ * BC_E_INVALID for bad sizes, pointers or d. */
+bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
+                          int d, float* out, void* workspace, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------ profiling */
+
+/* Kernel classes of the step and of populate, for bc_profile_* below. */
+enum {
+  BC_K_RMSNORM = 0,     /* RMSNorm (both norms of a layer) */
+  BC_K_QKV = 1,         /* fused Q/K/V projection + RoPE (+ cache write in populate) */
+  BC_K_ATTN_SHARED = 2, /* attention over [shared prefix ; own suffix] (layers l < d) */
+  BC_K_ATTN_FULL = 3,   /* full attention of each request (layers l >= d, populate) */
+  BC_K_OPROJ = 4,       /* output projection + residual add */
+  BC_K_GATE_UP = 5,     /* gate/up projection + SwiGLU */
+  BC_K_DOWN = 6,        /* down projection + residual add */
+  BC_K_OTHER = 7,       /* RoPE table, input widening, transition, suffix gather */
+  BC_K_COUNT = 8
+};
+
+/* Starts timing, with HIP events recorded on the launch stream around every
+ * later launch of a class whose bit (1u << class) is set in kernel_mask.
+ * Measurement only: the events add a small gap between kernels. */
+bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask);
+
+/* Waits for the recorded events, writes per class the summed kernel time in
+ * milliseconds (ms[BC_K_COUNT]) and the number of timed launches
+ * (launches[BC_K_COUNT]), then stops timing.  Either array may be NULL. */
+bc_status bc_profile_end(bc_model* model, double* ms, int* launches);
+
+/* ------------------------------------------------------- attention only */
+
+/* Shared-prefix bidirectional attention (Eq. 2 over [prefix ; own suffix], the
+ * shallow-layer form of Eq. 4), one launch:
+ *   out[b,j,i,:] = sum_t softmax_t(scale * q[b,j,i,:] . K_t) V_t
+ * over the keys t of [k_pre[g] ; k_suf[b,g]] with g = j / (Hq/Hkv); no mask.
+ *   q            bf16 [B, Hq, n_s, dh]
+ *   k_pre, v_pre bf16 [Hkv, m, dh]   one copy shared by all B requests (m >= 0)
+ *   k_suf, v_suf bf16 [B, Hkv, n_s, dh]
+ *   out          fp32 [B, Hq, n_s, dh]
+ * B, n_s >= 1; dh in {64, 128}; Hq % Hkv == 0.  Products use bf16 operands
+ * with fp32 accumulation; the softmax is fp32 (probabilities are rounded to
+ * bf16 for the P.V product). */
+bc_status bc_shared_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
+                                     const void* k_suf, const void* v_suf, float* out, int B,
+                                     int Hq, int Hkv, int m, int n_s, int dh, float scale,
+                                     void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* BICACHE_H */

@@ -1,0 +1,73 @@
+"""Builds libbicache.so (all HIP kernels + the C ABI) for gfx950, in-tree.
+
+    python -m paper_2606_07571_amd.build          # or: from ... import build; build.build()
+
+Objects are compiled in parallel with hipcc and linked into
+paper_2606_07571_amd/libbicache.so.  Also builds the host-only
+tests/native/libbicache_table_host.so (the FIFO table and the prefix-key hash
+compiled with the system C++ compiler, no HIP) used by the CPU tests.
+"""
+import concurrent.futures as cf
+import os
+import shutil
+import subprocess
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+ROOT = os.path.dirname(PKG)
+CSRC = os.path.join(PKG, "csrc")
+BUILD = os.path.join(PKG, "_build")
+LIB = os.path.join(PKG, "libbicache.so")
+HOST_LIB = os.path.join(ROOT, "tests", "native", "libbicache_table_host.so")
+
+HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
+ARCH = "gfx950"
+SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "runtime.cpp", "xxh64.cpp"]
+FLAGS = [
+    "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
+    # no packed-fp32 (v_pk_*_f32) instructions anywhere in device code
+    "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",
+    "-Wno-unused-command-line-argument",
+    f"-I{os.path.join(ROOT, 'include')}",
+]
+
+
+def _compile(src):
+    obj = os.path.join(BUILD, os.path.basename(src) + ".o")
+    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
+    if r.returncode != 0:
+        raise RuntimeError(f"compiling {src} failed:\n{err}")
+    return obj
+
+
+def build_host_lib():
+    os.makedirs(os.path.dirname(HOST_LIB), exist_ok=True)
+    cxx = shutil.which("g++") or "c++"
+    cmd = [cxx, "-O2", "-std=c++17", "-shared", "-fPIC", f"-I{CSRC}",
+           os.path.join(ROOT, "tests", "native", "table_shim.cpp"),
+           os.path.join(CSRC, "xxh64.cpp"), "-o", HOST_LIB]
+    subprocess.run(cmd, check=True)
+    return HOST_LIB
+
+
+def build(verbose=True):
+    os.makedirs(BUILD, exist_ok=True)
+    with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
+        objs = list(ex.map(_compile, SOURCES))
+    tmp = LIB + ".tmp"
+    cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"linking failed:\n{r.stderr}")
+    os.replace(tmp, LIB)
+    build_host_lib()
+    if verbose:
+        print(f"built {LIB}")
+    return LIB
+
+
+if __name__ == "__main__":
+    build()
+    sys.exit(0)

@@ -1,0 +1,151 @@
+// HBM-bound kernels of the step: RMSNorm (fp32 residual in, bf16 GEMM operand
+// out), the bf16 -> fp32 input widening, the transition at the reuse depth
+// (prefix rows from the cached residual broadcast to every request), the final
+// gather of the suffix rows, and the RoPE cos/sin table.
+//
+// All of them move 16-byte vectors per lane with consecutive lanes on
+// consecutive addresses, so every wave issues fully coalesced 1 KiB accesses.
+#include "device_common.hpp"
+#include "kernels.hpp"
+
+namespace bc {
+namespace {
+
+// One wave per row; each lane owns h/256 groups of 4 consecutive elements.
+// Sum of squares in fp32, reduced across the wave with xor shuffles.
+template <int VPL>  // float4 groups per lane
+__global__ void __launch_bounds__(256) rmsnorm_kernel(const float* __restrict__ x,
+                                                      const bf16* __restrict__ gain,
+                                                      bf16* __restrict__ out, int rows, int h,
+                                                      float eps) {
+  const int lane = threadIdx.x & 63;
+  const int row = blockIdx.x * 4 + (threadIdx.x >> 6);
+  if (row >= rows) return;
+  const f32x4* xr = reinterpret_cast<const f32x4*>(x + (long)row * h);
+  f32x4 v[VPL];
+  float ss = 0.f;
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int g = lane + i * 64;
+    if (g * 4 < h) {
+      v[i] = xr[g];
+      ss += v[i][0] * v[i][0] + v[i][1] * v[i][1] + v[i][2] * v[i][2] + v[i][3] * v[i][3];
+    }
+  }
+  ss = wave_sum(ss);
+  const float r = rsqrtf(ss / (float)h + eps);
+  u32x2* orow = reinterpret_cast<u32x2*>(out + (long)row * h);
+  const u32x2* gr = reinterpret_cast<const u32x2*>(gain);
+#pragma unroll
+  for (int i = 0; i < VPL; ++i) {
+    const int g = lane + i * 64;
+    if (g * 4 < h) {
+      const u32x2 gw = gr[g];
+      const float g0 = __builtin_bit_cast(float, gw[0] << 16), g1 = __builtin_bit_cast(float, gw[0] & 0xffff0000u);
+      const float g2 = __builtin_bit_cast(float, gw[1] << 16), g3 = __builtin_bit_cast(float, gw[1] & 0xffff0000u);
+      u32x2 o = {pack_bf16x2(v[i][0] * r * g0, v[i][1] * r * g1),
+                 pack_bf16x2(v[i][2] * r * g2, v[i][3] * r * g3)};
+      orow[g] = o;
+    }
+  }
+}
+
+__global__ void bf16_to_f32_kernel(const bf16* __restrict__ in, float* __restrict__ out, long n8) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= n8) return;
+  const u32x4 w = reinterpret_cast<const u32x4*>(in)[i];
+  f32x4 a, b;
+#pragma unroll
+  for (int k = 0; k < 2; ++k) {
+    a[2 * k] = __builtin_bit_cast(float, w[k] << 16);
+    a[2 * k + 1] = __builtin_bit_cast(float, w[k] & 0xffff0000u);
+    b[2 * k] = __builtin_bit_cast(float, w[2 + k] << 16);
+    b[2 * k + 1] = __builtin_bit_cast(float, w[2 + k] & 0xffff0000u);
+  }
+  reinterpret_cast<f32x4*>(out)[2 * i] = a;
+  reinterpret_cast<f32x4*>(out)[2 * i + 1] = b;
+}
+
+// grid.y = request b, grid.x covers the N*h/4 float4 of one request.
+__global__ void build_full_kernel(const f32x4* __restrict__ pre, const f32x4* __restrict__ suf,
+                                  f32x4* __restrict__ R, long pre4, long suf4) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long b = blockIdx.y;
+  if (i >= pre4 + suf4) return;
+  R[b * (pre4 + suf4) + i] = i < pre4 ? pre[i] : suf[b * suf4 + (i - pre4)];
+}
+
+__global__ void gather_suffix_kernel(const f32x4* __restrict__ R, f32x4* __restrict__ out,
+                                     long pre4, long suf4) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  const long b = blockIdx.y;
+  if (i >= suf4) return;
+  out[b * suf4 + i] = R[b * (pre4 + suf4) + pre4 + i];
+}
+
+// Angles in double: pos * theta^(-2i/dh) reaches ~1e4 rad, where an fp32
+// product would already carry ~1e-3 rad of error.
+__global__ void rope_table_kernel(float* cos_t, float* sin_t, int n_pos, int half, double theta) {
+  const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i >= (long)n_pos * half) return;
+  const int p = (int)(i / half), k = (int)(i % half);
+  const double inv_freq = pow(theta, -2.0 * k / (2.0 * half));
+  double sn, cs;
+  sincos((double)p * inv_freq, &sn, &cs);
+  cos_t[i] = (float)cs;
+  sin_t[i] = (float)sn;
+}
+
+}  // namespace
+
+hipError_t rmsnorm(const float* x, const void* gain, void* out, int rows, int h, float eps,
+                   hipStream_t s) {
+  if (rows == 0) return hipSuccess;
+  const int vpl = (h + 255) / 256;
+  const dim3 grid((rows + 3) / 4), block(256);
+  // VPL float4 groups per lane, the next power of two >= h/256 (h <= 8192)
+#define BC_RMS(V) hipLaunchKernelGGL(rmsnorm_kernel<V>, grid, block, 0, s, x, (const bf16*)gain, \
+                                     (bf16*)out, rows, h, eps)
+  if (vpl <= 1) BC_RMS(1);
+  else if (vpl <= 2) BC_RMS(2);
+  else if (vpl <= 4) BC_RMS(4);
+  else if (vpl <= 8) BC_RMS(8);
+  else if (vpl <= 16) BC_RMS(16);
+  else BC_RMS(32);
+#undef BC_RMS
+  return hipGetLastError();
+}
+
+hipError_t bf16_to_f32(const void* in, float* out, long n, hipStream_t s) {
+  const long n8 = n / 8;
+  if (n8 == 0) return hipSuccess;
+  hipLaunchKernelGGL(bf16_to_f32_kernel, dim3((unsigned)((n8 + 255) / 256)), dim3(256), 0, s,
+                     (const bf16*)in, out, n8);
+  return hipGetLastError();
+}
+
+hipError_t build_full_residual(const float* pre, const float* suf, float* R, int B, int m,
+                               int n_s, int h, hipStream_t s) {
+  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4;
+  hipLaunchKernelGGL(build_full_kernel, dim3((unsigned)((pre4 + suf4 + 255) / 256), B), dim3(256),
+                     0, s, (const f32x4*)pre, (const f32x4*)suf, (f32x4*)R, pre4, suf4);
+  return hipGetLastError();
+}
+
+hipError_t gather_suffix(const float* R, float* out, int B, int m, int n_s, int h,
+                         hipStream_t s) {
+  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4;
+  hipLaunchKernelGGL(gather_suffix_kernel, dim3((unsigned)((suf4 + 255) / 256), B), dim3(256), 0,
+                     s, (const f32x4*)R, (f32x4*)out, pre4, suf4);
+  return hipGetLastError();
+}
+
+hipError_t rope_table(float* cos_t, float* sin_t, int n_pos, int dh, double theta,
+                      hipStream_t s) {
+  const long n = (long)n_pos * (dh / 2);
+  hipLaunchKernelGGL(rope_table_kernel, dim3((unsigned)((n + 255) / 256)), dim3(256), 0, s, cos_t,
+                     sin_t, n_pos, dh / 2, theta);
+  return hipGetLastError();
+}
+
+}  // namespace bc

@@ -1,0 +1,74 @@
+// Host-side launchers of the gfx950 kernels.  Every launcher enqueues on
+// `stream` and returns the hipError_t of the launch.  Shapes are validated by
+// the caller (runtime.cpp) before any launcher runs.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace bc {
+
+// ----- GEMM family: C = A[M,K] . W[N,K]^T, bf16 operands, fp32 accumulation.
+
+// R[M, N] (fp32, row stride ldr) += A . W^T
+hipError_t gemm_residual(const void* A, int lda, const void* W, int ldw, int M, int N, int K,
+                         float* R, int ldr, hipStream_t s);
+
+// act[M, F] (bf16) = silu(A . Wg^T) * (A . Wu^T), Wg = W rows [0, F), Wu = rows [F, 2F)
+hipError_t gemm_swiglu(const void* A, int lda, const void* W, int ldw, int M, int F, int K,
+                       void* act, hipStream_t s);
+
+// Fused Q/K/V projection with rotate-half RoPE.  Row r of A is token
+// t = r % n_seq of sequence b = r / n_seq at position pos0 + t.  Output column
+// block j of W (head j, dh rows) goes to Q head j (j < Hq), K head j - Hq
+// (j < Hq + Hkv) or V head j - Hq - Hkv; element (b, head, t, dim) of a part is
+// stored at base + b*sb + head*sh + t*dh + dim (bf16).  Q and K are rotated
+// with the tables cos_t/sin_t [pos][dh/2].
+struct QkvOut {
+  void* q;
+  void* k;
+  void* v;
+  long q_sb, q_sh, k_sb, k_sh, v_sb, v_sh;
+};
+hipError_t gemm_qkv_rope(const void* A, int lda, const void* W, int ldw, int M, int K, int Hq,
+                         int Hkv, int dh, int n_seq, int pos0, const float* cos_t,
+                         const float* sin_t, const QkvOut& out, hipStream_t s);
+
+// ----- attention: one launch of shared-prefix bidirectional attention.
+// Prefix K/V [Hkv][m][dh] (head stride p_sh elements, rows dh apart) are shared
+// by every request; suffix K/V are per request.  m may be 0 (plain full
+// attention of each request over its own n_s keys).
+struct AttnArgs {
+  const void* q;
+  long q_sb, q_sh, q_sr;
+  const void* kp;
+  const void* vp;
+  long p_sh;
+  const void* ks;
+  const void* vs;
+  long s_sb, s_sh, s_sr;
+  void* out;
+  long o_sb, o_sh, o_sr;
+  int B, Hq, Hkv, m, n_s, dh;
+  float scale;
+  int out_f32;  // 1: fp32 output, 0: bf16 output
+};
+hipError_t attention(const AttnArgs& a, hipStream_t s);
+
+// ----- elementwise / normalisation
+// out[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gain)
+hipError_t rmsnorm(const float* x, const void* gain, void* out, int rows, int h, float eps,
+                   hipStream_t s);
+// out[i] = float(in[i])
+hipError_t bf16_to_f32(const void* in, float* out, long n, hipStream_t s);
+// R[b, t, :] = t < m ? pre[t, :] : suf[b, t - m, :]   (all fp32, row length h)
+hipError_t build_full_residual(const float* pre, const float* suf, float* R, int B, int m,
+                               int n_s, int h, hipStream_t s);
+// out[b, t, :] = R[b, m + t, :]
+hipError_t gather_suffix(const float* R, float* out, int B, int m, int n_s, int h,
+                         hipStream_t s);
+// cos_t/sin_t[p, i] = cos/sin(p * theta^(-2i/dh)), p in [0, n_pos), i in [0, dh/2)
+hipError_t rope_table(float* cos_t, float* sin_t, int n_pos, int dh, double theta,
+                      hipStream_t s);
+
+}  // namespace bc

@@ -1,0 +1,556 @@
+// Host runtime and C ABI of libbicache.so: argument validation, the KV store H
+// with FIFO eviction, cache-entry and workspace layouts, and the layer loops
+// of populate (prefix-only forward) and of the step at reuse depth d.
+//
+// Every device buffer is the caller's; this file only carves caller-provided
+// workspace into sub-buffers and enqueues kernels on the caller's stream.
+#include <hip/hip_runtime.h>
+#include <stdarg.h>
+#include <stdio.h>
+
+#include <climits>
+#include <cstdint>
+#include <new>
+#include <string>
+#include <vector>
+
+#include "../../include/bicache.h"
+#include "cache_table.hpp"
+#include "kernels.hpp"
+
+// HIP-event timing of selected kernel classes (bc_profile_*).
+struct Profiler {
+  unsigned mask = 0;
+  std::vector<hipEvent_t> pool;  // reused across sessions, destroyed with the model
+  size_t used = 0;
+  struct Rec {
+    int kind;
+    size_t start, stop;
+  };
+  std::vector<Rec> recs;
+};
+
+struct bc_model {
+  bc_model_config cfg;
+  std::vector<bc_layer_weights> layers;
+  bc::CacheTable table;
+  Profiler prof;
+  bc_model(const bc_model_config& c, const bc_layer_weights* l, int cap)
+      : cfg(c), layers(l, l + c.n_layers), table(cap) {}
+  ~bc_model() {
+    for (hipEvent_t e : prof.pool) (void)hipEventDestroy(e);
+  }
+};
+
+namespace {
+
+thread_local std::string g_err;
+
+bc_status fail(bc_status st, const char* fmt, ...) {
+  char buf[512];
+  va_list ap;
+  va_start(ap, fmt);
+  vsnprintf(buf, sizeof buf, fmt, ap);
+  va_end(ap);
+  g_err = buf;
+  return st;
+}
+
+bc_status ok() {
+  g_err.clear();
+  return BC_OK;
+}
+
+constexpr size_t kAlign = 256;
+size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
+
+// Sub-buffer plan of a workspace.  All offsets are 256-byte aligned.
+struct Plan {
+  size_t cos = 0, sin = 0, xn = 0, q = 0, k = 0, v = 0, ao = 0, act = 0, R = 0, total = 0;
+};
+
+struct Bump {
+  size_t at = 0;
+  size_t take(size_t bytes) {
+    const size_t o = at;
+    at = align_up(at + bytes);
+    return o;
+  }
+};
+
+// rows: token rows a layer processes at most; n_pos: RoPE table positions;
+// with_kv: K/V live in the workspace (step) rather than in the cache (populate);
+// resid_rows: rows of the fp32 residual kept in the workspace (0 = none).
+Plan make_plan(const bc_model_config& c, long rows, long n_pos, bool with_kv, long resid_rows) {
+  Plan p;
+  Bump b;
+  const long hd = (long)c.n_heads * c.head_dim, kvd = (long)c.n_kv_heads * c.head_dim;
+  p.cos = b.take(n_pos * (c.head_dim / 2) * 4);
+  p.sin = b.take(n_pos * (c.head_dim / 2) * 4);
+  p.xn = b.take(rows * c.hidden * 2);
+  p.q = b.take(rows * hd * 2);
+  if (with_kv) {
+    p.k = b.take(rows * kvd * 2);
+    p.v = b.take(rows * kvd * 2);
+  }
+  p.ao = b.take(rows * hd * 2);
+  p.act = b.take(rows * (long)c.ffn * 2);
+  if (resid_rows) p.R = b.take(resid_rows * c.hidden * 4);
+  p.total = b.at;
+  return p;
+}
+
+// Cache entry layout: KV$ [Lc][2][Hkv][m][dh] bf16, then H$ [nH][m][h] fp32.
+struct EntryLayout {
+  size_t kv_layer = 0;  // bytes of one layer's K or V block
+  size_t h_off = 0, h_layer = 0, total = 0;
+  int n_h = 0;
+};
+
+EntryLayout entry_layout(const bc_model_config& c, int m, int Lc) {
+  EntryLayout e;
+  e.kv_layer = (size_t)c.n_kv_heads * m * c.head_dim * 2;
+  e.h_off = align_up((size_t)Lc * 2 * e.kv_layer);
+  e.n_h = Lc + 1 < c.n_layers ? Lc + 1 : c.n_layers;
+  e.h_layer = (size_t)m * c.hidden * 4;
+  e.total = e.h_off + (size_t)e.n_h * e.h_layer;
+  return e;
+}
+
+bool config_ok(const bc_model_config& c, std::string* why) {
+  char buf[256];
+  auto bad = [&](const char* s) {
+    snprintf(buf, sizeof buf, "invalid model config: %s", s);
+    *why = buf;
+    return false;
+  };
+  if (c.n_layers < 1) return bad("n_layers must be >= 1");
+  if (c.hidden < 64 || c.hidden % 64 || c.hidden > 8192) return bad("hidden must be a multiple of 64 in [64, 8192]");
+  if (c.head_dim != 64 && c.head_dim != 128) return bad("head_dim must be 64 or 128");
+  if (c.n_heads < 1 || c.n_kv_heads < 1 || c.n_heads % c.n_kv_heads)
+    return bad("n_heads must be a positive multiple of n_kv_heads");
+  if (c.ffn < 64 || c.ffn % 64) return bad("ffn must be a positive multiple of 64");
+  if (!(c.rms_eps >= 0.f) || !(c.rope_theta > 0.f)) return bad("rms_eps >= 0 and rope_theta > 0 required");
+  return true;
+}
+
+#define BC_HIP(expr)                                                                 \
+  do {                                                                               \
+    hipError_t e_ = (expr);                                                          \
+    if (e_ != hipSuccess)                                                            \
+      return fail(BC_E_HIP, "%s failed: %s", #expr, hipGetErrorString(e_));          \
+  } while (0)
+
+// Records an event on `s` if class `kind` is being timed; returns its pool
+// index in *idx (or SIZE_MAX when not timing).
+hipError_t prof_mark(bc_model* mdl, int kind, hipStream_t s, size_t* idx) {
+  *idx = SIZE_MAX;
+  Profiler& p = mdl->prof;
+  if (!(p.mask & (1u << kind))) return hipSuccess;
+  if (p.used == p.pool.size()) {
+    hipEvent_t e;
+    hipError_t err = hipEventCreate(&e);
+    if (err != hipSuccess) return err;
+    p.pool.push_back(e);
+  }
+  *idx = p.used++;
+  return hipEventRecord(p.pool[*idx], s);
+}
+
+// Launch `expr` (a hipError_t expression), timed as class `kind` when enabled.
+#define BC_LAUNCH(mdl, kind, s, expr)                                             \
+  do {                                                                           \
+    size_t i0_, i1_;                                                             \
+    BC_HIP(prof_mark(mdl, kind, s, &i0_));                                       \
+    BC_HIP(expr);                                                                \
+    BC_HIP(prof_mark(mdl, kind, s, &i1_));                                       \
+    if (i0_ != SIZE_MAX) mdl->prof.recs.push_back({kind, i0_, i1_});             \
+  } while (0)
+
+// One transformer layer over `rows` = n_req * n_seq token rows held in the fp32
+// residual R.  Row r is token t = r % n_seq of request r / n_seq at RoPE
+// position pos0 + t.  The layer's own K/V are written to k_dst/v_dst
+// (element (req, head, t, dim) at req*kv_sb + head*kv_sh + t*dh + dim).
+// Attention of every request runs over [kp/vp (m_pre shared prefix rows, may be
+// 0) ; its own n_seq keys].
+struct LayerCall {
+  float* R;
+  int n_req, n_seq, pos0;
+  const void* kp;
+  const void* vp;
+  int m_pre;
+  void* k_dst;
+  void* v_dst;
+  long kv_sb, kv_sh;
+};
+
+bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const Plan& p,
+                    hipStream_t s) {
+  const bc_model_config& c = mdl->cfg;
+  const bc_layer_weights& w = mdl->layers[l];
+  const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
+  const int rows = lc.n_req * lc.n_seq;
+  const int hd = Hq * dh;
+  void* xn = ws + p.xn;
+  void* q = ws + p.q;
+  void* ao = ws + p.ao;
+  void* act = ws + p.act;
+  const float* cos_t = (const float*)(ws + p.cos);
+  const float* sin_t = (const float*)(ws + p.sin);
+
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.attn_norm, xn, rows, h, c.rms_eps, s));
+  bc::QkvOut qo{q, lc.k_dst, lc.v_dst, (long)Hq * lc.n_seq * dh, (long)lc.n_seq * dh,
+                lc.kv_sb, lc.kv_sh, lc.kv_sb, lc.kv_sh};
+  BC_LAUNCH(mdl, BC_K_QKV, s,
+            bc::gemm_qkv_rope(xn, h, w.w_qkv, h, rows, h, Hq, Hkv, dh, lc.n_seq, lc.pos0, cos_t,
+                              sin_t, qo, s));
+  bc::AttnArgs a{};
+  a.q = q;
+  a.q_sb = (long)Hq * lc.n_seq * dh;
+  a.q_sh = (long)lc.n_seq * dh;
+  a.q_sr = dh;
+  a.kp = lc.kp;
+  a.vp = lc.vp;
+  a.p_sh = (long)lc.m_pre * dh;
+  a.ks = lc.k_dst;
+  a.vs = lc.v_dst;
+  a.s_sb = lc.kv_sb;
+  a.s_sh = lc.kv_sh;
+  a.s_sr = dh;
+  a.out = ao;  // token-major [req, t, head, dim]: the O projection's A operand
+  a.o_sb = (long)lc.n_seq * hd;
+  a.o_sh = dh;
+  a.o_sr = hd;
+  a.B = lc.n_req;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.m = lc.m_pre;
+  a.n_s = lc.n_seq;
+  a.dh = dh;
+  a.scale = 1.f / sqrtf((float)dh);
+  a.out_f32 = 0;
+  BC_LAUNCH(mdl, lc.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
+  BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, lc.R, h, s));
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.ffn_norm, xn, rows, h, c.rms_eps, s));
+  BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
+  BC_LAUNCH(mdl, BC_K_DOWN, s, bc::gemm_residual(act, F, w.w_down, F, rows, h, F, lc.R, h, s));
+  return BC_OK;
+}
+
+bool step_shape_ok(const bc_model_config& c, int m, int B, int n_s, int d, std::string* why) {
+  char buf[256];
+  if (m < 1 || B < 1 || n_s < 1) {
+    snprintf(buf, sizeof buf, "m, B and n_s must be >= 1 (got m=%d B=%d n_s=%d)", m, B, n_s);
+    *why = buf;
+    return false;
+  }
+  if (d < 0 || d > c.n_layers) {
+    snprintf(buf, sizeof buf, "reuse depth d=%d outside [0, L=%d]", d, c.n_layers);
+    *why = buf;
+    return false;
+  }
+  const long N = (long)m + n_s;
+  const long rows = (long)B * N;
+  const long widest = c.ffn > (long)c.n_heads * c.head_dim ? c.ffn : (long)c.n_heads * c.head_dim;
+  if (N > INT_MAX / 2 || rows > INT_MAX / 2 || rows * (widest > c.hidden ? widest : c.hidden) > (1L << 40)) {
+    snprintf(buf, sizeof buf, "step too large (B=%d, m+n_s=%ld)", B, N);
+    *why = buf;
+    return false;
+  }
+  return true;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char* bc_last_error(void) { return g_err.c_str(); }
+
+bc_status bc_model_create(const bc_model_config* cfg, const bc_layer_weights* layers,
+                          int cache_capacity, bc_model** out) {
+  if (!cfg || !layers || !out) return fail(BC_E_INVALID, "null argument");
+  std::string why;
+  if (!config_ok(*cfg, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  if (cache_capacity < 1) return fail(BC_E_INVALID, "cache_capacity must be >= 1");
+  for (int l = 0; l < cfg->n_layers; ++l) {
+    const bc_layer_weights& w = layers[l];
+    if (!w.w_qkv || !w.w_o || !w.w_gate_up || !w.w_down || !w.attn_norm || !w.ffn_norm)
+      return fail(BC_E_INVALID, "layer %d has a null weight pointer", l);
+  }
+  bc_model* m = new (std::nothrow) bc_model(*cfg, layers, cache_capacity);
+  if (!m) return fail(BC_E_OOM, "host allocation of the model failed");
+  *out = m;
+  return ok();
+}
+
+bc_status bc_model_destroy(bc_model* model) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  delete model;
+  return ok();
+}
+
+size_t bc_prefix_cache_bytes(const bc_model* model, int m, int n_layers_to_cache) {
+  if (!model || m < 1 || n_layers_to_cache < 0 || n_layers_to_cache > model->cfg.n_layers) return 0;
+  return entry_layout(model->cfg, m, n_layers_to_cache).total;
+}
+
+size_t bc_cache_offset(const bc_model* model, int m, int Lc, int layer, int part, int head,
+                       int pos, int dim) {
+  const size_t bad = (size_t)-1;
+  if (!model || m < 1 || Lc < 0 || Lc > model->cfg.n_layers) return bad;
+  const bc_model_config& c = model->cfg;
+  const EntryLayout e = entry_layout(c, m, Lc);
+  if (pos < 0 || pos >= m || dim < 0) return bad;
+  if (part == 0 || part == 1) {
+    if (layer < 0 || layer >= Lc || head < 0 || head >= c.n_kv_heads || dim >= c.head_dim) return bad;
+    return ((size_t)(layer * 2 + part)) * e.kv_layer +
+           (((size_t)head * m + pos) * c.head_dim + dim) * 2;
+  }
+  if (part == 2) {
+    if (layer < 0 || layer >= e.n_h || dim >= c.hidden) return bad;
+    return e.h_off + (size_t)layer * e.h_layer + ((size_t)pos * c.hidden + dim) * 4;
+  }
+  return bad;
+}
+
+size_t bc_populate_workspace_bytes(const bc_model* model, int m) {
+  if (!model || m < 1) return 0;
+  return make_plan(model->cfg, m, m, false, m).total;
+}
+
+bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix, int m,
+                             int n_layers_to_cache, void* cache_mem, size_t cache_bytes,
+                             void* workspace, size_t ws_bytes, void* stream,
+                             uint64_t* evicted_key, int* evicted) {
+  if (evicted) *evicted = 0;
+  if (evicted_key) *evicted_key = 0;
+  if (!model || !x_prefix || !cache_mem || !workspace) return fail(BC_E_INVALID, "null argument");
+  const bc_model_config& c = model->cfg;
+  const int Lc = n_layers_to_cache;
+  if (m < 1) return fail(BC_E_INVALID, "prefix length m=%d must be >= 1", m);
+  if (Lc < 0 || Lc > c.n_layers) return fail(BC_E_INVALID, "n_layers_to_cache=%d outside [0, %d]", Lc, c.n_layers);
+  std::string why;
+  if (!step_shape_ok(c, m, 1, 1, 0, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  const EntryLayout e = entry_layout(c, m, Lc);
+  if (cache_bytes < e.total) return fail(BC_E_INVALID, "cache_bytes %zu < required %zu", cache_bytes, e.total);
+  if ((uintptr_t)cache_mem % kAlign) return fail(BC_E_INVALID, "cache_mem must be 256-byte aligned");
+  const Plan p = make_plan(c, m, m, false, m);
+  if (ws_bytes < p.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, p.total);
+  if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
+  if (model->table.contains(key)) return fail(BC_E_STATE, "key %016llx is already cached", (unsigned long long)key);
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  char* cm = (char*)cache_mem;
+  float* R = (float*)(ws + p.R);
+  const long mh = (long)m * c.hidden;
+  BC_LAUNCH(model, BC_K_OTHER, s,
+            bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), m, c.head_dim, c.rope_theta, s));
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_prefix, R, mh, s));
+  for (int l = 0; l < Lc || l < e.n_h; ++l) {
+    if (l < e.n_h)  // H$[l]: residual entering layer l of the prefix-only forward
+      BC_HIP(hipMemcpyAsync(cm + e.h_off + (size_t)l * e.h_layer, R, e.h_layer, hipMemcpyDeviceToDevice, s));
+    if (l >= Lc) break;
+    char* k_dst = cm + (size_t)(2 * l) * e.kv_layer;
+    char* v_dst = cm + (size_t)(2 * l + 1) * e.kv_layer;
+    LayerCall lc{R, 1, m, 0, nullptr, nullptr, 0, k_dst, v_dst, 0, (long)m * c.head_dim};
+    bc_status st = run_layer(model, l, lc, ws, p, s);
+    if (st != BC_OK) return st;
+  }
+  bc::CacheEntry ce;
+  ce.m = m;
+  ce.n_layers = Lc;
+  ce.mem = cache_mem;
+  ce.bytes = cache_bytes;
+  uint64_t ev = 0;
+  const bool did = model->table.insert(key, ce, &ev);
+  if (did) {
+    if (evicted) *evicted = 1;
+    if (evicted_key) *evicted_key = ev;
+  }
+  return ok();
+}
+
+bc_status bc_prefix_lookup(const bc_model* model, uint64_t key, int* m_out, int* n_layers_out) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  const bc::CacheEntry* e = model->table.find(key);
+  if (!e) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
+  if (m_out) *m_out = e->m;
+  if (n_layers_out) *n_layers_out = e->n_layers;
+  return ok();
+}
+
+bc_status bc_prefix_invalidate(bc_model* model, uint64_t key) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  if (!model->table.erase(key)) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
+  return ok();
+}
+
+bc_status bc_cache_keys(const bc_model* model, uint64_t* keys, int max_keys, int* n_out) {
+  if (!model || !n_out || max_keys < 0 || (max_keys > 0 && !keys)) return fail(BC_E_INVALID, "bad argument");
+  int i = 0;
+  for (uint64_t k : model->table.order()) {
+    if (i < max_keys) keys[i] = k;
+    ++i;
+  }
+  *n_out = i;
+  return ok();
+}
+
+uint64_t bc_prefix_key(const int32_t* token_ids, size_t n) {
+  // little-endian int32 bytes, independent of the host's byte order
+  std::vector<unsigned char> bytes(n * 4);
+  for (size_t i = 0; i < n; ++i) {
+    const uint32_t v = (uint32_t)token_ids[i];
+    for (int b = 0; b < 4; ++b) bytes[i * 4 + b] = (unsigned char)(v >> (8 * b));
+  }
+  return bc::xxh64(bytes.data(), bytes.size(), 0);
+}
+
+size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int d) {
+  if (!model) return 0;
+  std::string why;
+  if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return 0;
+  const int L = model->cfg.n_layers;
+  const long N = (long)m + n_s;
+  const long rows = (long)B * (d < L ? N : n_s);
+  return make_plan(model->cfg, rows, N, true, d < L ? (long)B * N : 0).total;
+}
+
+bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int* rows,
+                       int* pos_base, int* reads_kv, int* reads_h) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  std::string why;
+  if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  const int L = model->cfg.n_layers;
+  for (int l = 0; l < L; ++l) {
+    const bool shallow = l < d;
+    if (rows) rows[l] = shallow ? B * n_s : B * (m + n_s);
+    if (pos_base) pos_base[l] = shallow ? m : 0;
+    if (reads_kv) reads_kv[l] = shallow ? 1 : 0;
+  }
+  if (reads_h) *reads_h = d < L ? d : -1;
+  return ok();
+}
+
+bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
+                          int d, float* out, void* workspace, size_t ws_bytes, void* stream) {
+  if (!model || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+  const bc_model_config& c = model->cfg;
+  const int L = c.n_layers;
+  const bc::CacheEntry* ent = model->table.find(key);
+  if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
+  const int m = ent->m;
+  std::string why;
+  if (!step_shape_ok(c, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  if (d > ent->n_layers)
+    return fail(BC_E_INVALID, "reuse depth d=%d exceeds the %d cached layers of this prefix", d, ent->n_layers);
+  const long N = (long)m + n_s;
+  const long rows_max = (long)B * (d < L ? N : n_s);
+  const Plan p = make_plan(c, rows_max, N, true, d < L ? (long)B * N : 0);
+  if (ws_bytes < p.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, p.total);
+  if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  const char* cm = (const char*)ent->mem;
+  const EntryLayout e = entry_layout(c, m, ent->n_layers);
+  const int dh = c.head_dim, Hkv = c.n_kv_heads;
+
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), (int)N, dh, c.rope_theta, s));
+  // shallow residual: the suffix rows only, kept in `out`
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_suffix, out, (long)B * n_s * c.hidden, s));
+  for (int l = 0; l < d; ++l) {
+    LayerCall lc{out, B, n_s, m,
+                 cm + (size_t)(2 * l) * e.kv_layer, cm + (size_t)(2 * l + 1) * e.kv_layer, m,
+                 ws + p.k, ws + p.v, (long)Hkv * n_s * dh, (long)n_s * dh};
+    bc_status st = run_layer(model, l, lc, ws, p, s);
+    if (st != BC_OK) return st;
+  }
+  if (d < L) {
+    float* R = (float*)(ws + p.R);
+    const float* hd = (const float*)(cm + e.h_off + (size_t)d * e.h_layer);
+    BC_LAUNCH(model, BC_K_OTHER, s, bc::build_full_residual(hd, out, R, B, m, n_s, c.hidden, s));
+    for (int l = d; l < L; ++l) {
+      LayerCall lc{R, B, (int)N, 0, nullptr, nullptr, 0,
+                   ws + p.k, ws + p.v, (long)Hkv * N * dh, N * dh};
+      bc_status st = run_layer(model, l, lc, ws, p, s);
+      if (st != BC_OK) return st;
+    }
+    BC_LAUNCH(model, BC_K_OTHER, s, bc::gather_suffix(R, out, B, m, n_s, c.hidden, s));
+  }
+  return ok();
+}
+
+bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  model->prof.mask = kernel_mask;
+  model->prof.used = 0;
+  model->prof.recs.clear();
+  return ok();
+}
+
+bc_status bc_profile_end(bc_model* model, double* ms, int* launches) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  Profiler& p = model->prof;
+  p.mask = 0;
+  double acc[BC_K_COUNT] = {0};
+  int cnt[BC_K_COUNT] = {0};
+  if (p.used) BC_HIP(hipEventSynchronize(p.pool[p.used - 1]));
+  for (const Profiler::Rec& r : p.recs) {
+    float t = 0.f;
+    BC_HIP(hipEventElapsedTime(&t, p.pool[r.start], p.pool[r.stop]));
+    acc[r.kind] += t;
+    cnt[r.kind] += 1;
+  }
+  p.recs.clear();
+  p.used = 0;
+  for (int k = 0; k < BC_K_COUNT; ++k) {
+    if (ms) ms[k] = acc[k];
+    if (launches) launches[k] = cnt[k];
+  }
+  return ok();
+}
+
+bc_status bc_shared_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
+                                     const void* k_suf, const void* v_suf, float* out, int B,
+                                     int Hq, int Hkv, int m, int n_s, int dh, float scale,
+                                     void* stream) {
+  if (!q || !k_suf || !v_suf || !out || (m > 0 && (!k_pre || !v_pre)))
+    return fail(BC_E_INVALID, "null argument");
+  if (B < 1 || n_s < 1 || m < 0) return fail(BC_E_INVALID, "B, n_s >= 1 and m >= 0 required");
+  if (dh != 64 && dh != 128) return fail(BC_E_INVALID, "dh must be 64 or 128 (got %d)", dh);
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv) return fail(BC_E_INVALID, "Hq must be a positive multiple of Hkv");
+  if ((long)B * Hq * ((n_s + 31) / 32) > INT_MAX / 2 || (long)m * dh > INT_MAX / 2 ||
+      (long)n_s * dh > INT_MAX / 2)
+    return fail(BC_E_CAPACITY, "attention problem too large");
+  bc::AttnArgs a{};
+  a.q = q;
+  a.q_sb = (long)Hq * n_s * dh;
+  a.q_sh = (long)n_s * dh;
+  a.q_sr = dh;
+  a.kp = k_pre;
+  a.vp = v_pre;
+  a.p_sh = (long)m * dh;
+  a.ks = k_suf;
+  a.vs = v_suf;
+  a.s_sb = (long)Hkv * n_s * dh;
+  a.s_sh = (long)n_s * dh;
+  a.s_sr = dh;
+  a.out = out;
+  a.o_sb = (long)Hq * n_s * dh;
+  a.o_sh = (long)n_s * dh;
+  a.o_sr = dh;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.m = m;
+  a.n_s = n_s;
+  a.dh = dh;
+  a.scale = scale;
+  a.out_f32 = 1;
+  BC_HIP(bc::attention(a, (hipStream_t)stream));
+  return ok();
+}
+
+}  // extern "C"

@@ -1,0 +1,217 @@
+"""Host-side checks of the C ABI (no GPU): exports, argument validation, key
+hash, cache layout offsets, step work accounting, FIFO bookkeeping."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+import xxhash
+
+from oracle.cache_table import FifoTable
+from oracle.xxh64 import prefix_key as oracle_prefix_key
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "bicache.h")
+
+pytest.importorskip("torch")
+import paper_2606_07571_amd as bc  # noqa: E402
+from paper_2606_07571_amd import _lib  # noqa: E402
+
+
+def _declared_symbols():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(bc_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_library_exports_every_declared_symbol():
+    L = bc.lib()
+    syms = _declared_symbols()
+    assert len(syms) >= 15
+    for s in syms:
+        assert hasattr(L, s), f"{s} not exported"
+
+
+def test_prefix_key_matches_xxhash_and_oracle():
+    rng = np.random.default_rng(0)
+    for n in (0, 1, 7, 8, 9, 31, 32, 33, 1536, 8192):
+        ids = rng.integers(-2**31, 2**31 - 1, size=n)
+        k = bc.prefix_key(ids)
+        assert k == xxhash.xxh64_intdigest(ids.astype("<i4").tobytes(), seed=0)
+        if n <= 64:
+            assert k == oracle_prefix_key(ids)
+
+
+CFG = dict(n_layers=3, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=512,
+           rms_eps=1e-5, rope_theta=500000.0)
+FAKE = 1 << 20      # a non-null fake device address: never dereferenced by these calls
+
+
+def _fake_layers(n):
+    return [{k: None for k in _lib._WEIGHT_KEYS} for _ in range(n)]
+
+
+def _model(cfg=CFG, cap=4):
+    arr = (_lib.LayerWeights * cfg["n_layers"])()
+    for i in range(cfg["n_layers"]):
+        for k in _lib._WEIGHT_KEYS:
+            setattr(arr[i], k, FAKE)
+    c = _lib.ModelConfig(*[cfg[k] for k in ("n_layers", "hidden", "n_heads", "n_kv_heads",
+                                             "head_dim", "ffn", "rms_eps", "rope_theta")])
+    h = C.c_void_p()
+    st = bc.lib().bc_model_create(C.byref(c), arr, cap, C.byref(h))
+    return st, h
+
+
+def test_model_create_validation():
+    st, h = _model()
+    assert st == 0
+    assert bc.lib().bc_model_destroy(h) == 0
+    for bad in (dict(n_layers=0), dict(hidden=100), dict(head_dim=96), dict(n_kv_heads=3),
+                dict(ffn=100), dict(hidden=16384)):
+        st, _ = _model(dict(CFG, **bad))
+        assert st == -1, bad
+        assert "invalid model config" in bc.lib().bc_last_error().decode()
+    st, _ = _model(cap=0)
+    assert st == -1
+    # a null weight pointer
+    arr = (_lib.LayerWeights * 3)()
+    c = _lib.ModelConfig(3, 256, 4, 2, 64, 512, 1e-5, 5e5)
+    h = C.c_void_p()
+    assert bc.lib().bc_model_create(C.byref(c), arr, 2, C.byref(h)) == -1
+
+
+def test_cache_layout_offsets():
+    st, h = _model()
+    L = bc.lib()
+    m, Lc = 129, 2
+    Hkv, dh, hid = 2, 64, 256
+    kv_layer = Hkv * m * dh * 2
+    h_off = -(-(Lc * 2 * kv_layer) // 256) * 256
+    n_h = min(Lc + 1, 3)
+    assert L.bc_prefix_cache_bytes(h, m, Lc) == h_off + n_h * m * hid * 4
+    for (layer, part, head, pos, dim) in [(0, 0, 0, 0, 0), (1, 1, 1, 128, 63), (0, 1, 1, 5, 7)]:
+        exp = (layer * 2 + part) * kv_layer + ((head * m + pos) * dh + dim) * 2
+        assert L.bc_cache_offset(h, m, Lc, layer, part, head, pos, dim) == exp
+    for (layer, pos, dim) in [(0, 0, 0), (2, 128, 255), (1, 3, 4)]:
+        exp = h_off + layer * m * hid * 4 + (pos * hid + dim) * 4
+        assert L.bc_cache_offset(h, m, Lc, layer, 2, 0, pos, dim) == exp
+    bad = (1 << 64) - 1
+    assert L.bc_cache_offset(h, m, Lc, 2, 0, 0, 0, 0) == bad      # layer >= Lc
+    assert L.bc_cache_offset(h, m, Lc, 3, 2, 0, 0, 0) == bad      # H$ index > min(Lc, L-1)
+    assert L.bc_cache_offset(h, m, Lc, 0, 0, 2, 0, 0) == bad      # head >= Hkv
+    assert L.bc_cache_offset(h, m, Lc, 0, 0, 0, m, 0) == bad      # pos >= m
+    assert L.bc_cache_offset(h, m, Lc, 0, 3, 0, 0, 0) == bad      # no such part
+    assert L.bc_prefix_cache_bytes(h, 0, 1) == 0 and L.bc_prefix_cache_bytes(h, 4, 4) == 0
+    L.bc_model_destroy(h)
+
+
+def test_step_plan_accounting():
+    st, h = _model()
+    L = bc.lib()
+    m, B, n_s = 129, 3, 65
+    for d in range(4):
+        rows, pos, kv = (C.c_int * 3)(), (C.c_int * 3)(), (C.c_int * 3)()
+        rh = C.c_int()
+        assert L.bc_step_plan(h, m, B, n_s, d, rows, pos, kv, C.byref(rh)) == 0
+        assert list(rows) == [B * n_s if l < d else B * (m + n_s) for l in range(3)]
+        assert list(pos) == [m if l < d else 0 for l in range(3)]
+        assert list(kv) == [1 if l < d else 0 for l in range(3)]
+        assert rh.value == (d if d < 3 else -1)
+    assert L.bc_step_plan(h, m, B, n_s, 4, None, None, None, None) == -1
+    assert L.bc_step_plan(h, m, B, n_s, -1, None, None, None, None) == -1
+    assert L.bc_step_plan(h, m, 0, n_s, 1, None, None, None, None) == -1
+    # the workspace grows with the deep part
+    assert L.bc_step_workspace_bytes(h, m, B, n_s, 3) < L.bc_step_workspace_bytes(h, m, B, n_s, 0)
+    assert L.bc_step_workspace_bytes(h, m, B, n_s, 5) == 0
+    L.bc_model_destroy(h)
+
+
+def test_entry_point_validation_without_device_work():
+    st, h = _model(cap=2)
+    L = bc.lib()
+    ev, evk = C.c_int(7), C.c_uint64(7)
+    big = 1 << 40
+    # m = 0, Lc > L, short cache, misaligned cache, short workspace, null input
+    assert L.bc_prefix_populate(h, 1, FAKE, 0, 1, FAKE, big, FAKE, big, None, C.byref(evk), C.byref(ev)) == -1
+    assert ev.value == 0 and evk.value == 0
+    assert L.bc_prefix_populate(h, 1, FAKE, 8, 4, FAKE, big, FAKE, big, None, None, None) == -1
+    assert L.bc_prefix_populate(h, 1, FAKE, 8, 3, FAKE, 16, FAKE, big, None, None, None) == -1
+    assert L.bc_prefix_populate(h, 1, FAKE, 8, 3, FAKE + 8, big, FAKE, big, None, None, None) == -1
+    assert L.bc_prefix_populate(h, 1, FAKE, 8, 3, FAKE, big, FAKE, 16, None, None, None) == -1
+    assert L.bc_prefix_populate(h, 1, None, 8, 3, FAKE, big, FAKE, big, None, None, None) == -1
+    # nothing was inserted
+    n = C.c_int()
+    assert L.bc_cache_keys(h, None, 0, C.byref(n)) == 0 and n.value == 0
+    # miss paths
+    assert L.bc_step_forward(h, 1, FAKE, 2, 4, 1, FAKE, FAKE, big, None) == -2
+    assert "not cached" in L.bc_last_error().decode()
+    assert L.bc_prefix_lookup(h, 1, None, None) == -2
+    assert L.bc_prefix_invalidate(h, 1) == -2
+    # attention-only entry point
+    A = L.bc_shared_prefix_attention
+    assert A(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 8, 4, 96, 0.1, None) == -1   # dh
+    assert A(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 6, 4, 8, 4, 64, 0.1, None) == -1   # Hq % Hkv
+    assert A(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 0, 4, 4, 8, 4, 64, 0.1, None) == -1   # B
+    assert A(FAKE, None, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 8, 4, 64, 0.1, None) == -1   # null prefix, m > 0
+    L.bc_model_destroy(h)
+
+
+# ------------------------------------------------------------ FIFO bookkeeping
+
+@pytest.fixture(scope="module")
+def host_table():
+    path = os.path.join(ROOT, "tests", "native", "libbicache_table_host.so")
+    if not os.path.exists(path):
+        pytest.skip("host table library not built")
+    T = C.CDLL(path)
+    T.bct_create.restype = C.c_void_p
+    T.bct_create.argtypes = [C.c_int]
+    T.bct_destroy.argtypes = [C.c_void_p]
+    T.bct_insert.argtypes = [C.c_void_p, C.c_uint64, C.c_int, C.POINTER(C.c_uint64)]
+    T.bct_erase.argtypes = [C.c_void_p, C.c_uint64]
+    T.bct_lookup.argtypes = [C.c_void_p, C.c_uint64]
+    T.bct_keys.argtypes = [C.c_void_p, C.POINTER(C.c_uint64), C.c_int]
+    T.bct_xxh64.restype = C.c_uint64
+    T.bct_xxh64.argtypes = [C.c_void_p, C.c_uint64, C.c_uint64]
+    return T
+
+
+@pytest.mark.parametrize("cap", [1, 2, 5])
+def test_fifo_table_matches_model(host_table, cap):
+    T = host_table
+    t = T.bct_create(cap)
+    ref = FifoTable(cap)
+    rng = np.random.default_rng(cap)
+    keys = [int(x) for x in rng.integers(0, 2**64 - 1, size=12, dtype=np.uint64)]
+    for step in range(400):
+        k = keys[rng.integers(len(keys))]
+        op = rng.integers(3)
+        if op == 0:
+            ev = C.c_uint64()
+            r = T.bct_insert(t, k, step, C.byref(ev))
+            try:
+                e = ref.insert(k, step)
+                assert r == (1 if e is not None else 0)
+                if e is not None:
+                    assert ev.value == e
+            except KeyError:
+                assert r == -1
+        elif op == 1:
+            assert T.bct_erase(t, k) == (1 if ref.invalidate(k) else 0)
+        else:
+            meta = ref.lookup(k)
+            assert T.bct_lookup(t, k) == (-1 if meta is None else meta)
+        buf = (C.c_uint64 * 16)()
+        n = T.bct_keys(t, buf, 16)
+        assert [buf[i] for i in range(n)] == ref.order()
+    T.bct_destroy(t)
+
+
+def test_native_xxh64_matches_library(host_table):
+    rng = np.random.default_rng(9)
+    for n in list(range(0, 80)) + [1000]:
+        data = rng.integers(0, 256, size=n, dtype=np.uint8).tobytes()
+        for seed in (0, 12345):
+            assert host_table.bct_xxh64(data, n, seed) == xxhash.xxh64_intdigest(data, seed=seed)

@@ -1,0 +1,149 @@
+"""GPU parity of populate and of the step at every reuse depth d against the
+fp64 oracle, plus the store's bookkeeping driven through real populates."""
+import numpy as np
+import pytest
+import torch
+
+from oracle import transformer as OT
+from oracle.cache_table import FifoTable
+import paper_2606_07571_amd as bc
+from paper_2606_07571_amd import synth
+from paper_2606_07571_amd.synth import to_f64, weights_f64
+from tests.parity import assert_close, assert_close_bf16_store, say
+
+pytestmark = pytest.mark.gpu
+
+SMALL = [
+    # GQA, dh 64, ragged m and n_s
+    dict(cfg=synth.model_config(n_layers=3, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=512),
+         m=129, n_s=65, B=3, seed=11),
+    # MHA, dh 128
+    dict(cfg=synth.model_config(n_layers=2, hidden=512, n_heads=4, n_kv_heads=4, head_dim=128, ffn=1024),
+         m=100, n_s=37, B=2, seed=12),
+    # Dream-like grouping (7 query heads per KV head), tiny suffix
+    dict(cfg=synth.model_config(n_layers=2, hidden=896, n_heads=7, n_kv_heads=1, head_dim=128, ffn=640),
+         m=70, n_s=1, B=4, seed=13),
+]
+
+
+class Setup:
+    def __init__(self, spec):
+        self.spec = spec
+        cfg = spec["cfg"]
+        self.cfg = cfg
+        self.w_cpu = synth.model_weights(cfg, 1000 * spec["seed"])
+        self.w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in self.w_cpu]
+        self.xp, self.xs = synth.step_inputs(cfg, spec["B"], spec["m"], spec["n_s"], 1000 * spec["seed"] + 500)
+        self.w64 = weights_f64(self.w_cpu)
+        self.model = bc.Model(cfg, self.w_dev, cache_capacity=4)
+        self.key = bc.prefix_key(np.arange(spec["m"]))
+        say(f"populate {cfg} m={spec['m']}")
+        self.model.populate(self.key, self.xp.cuda(), cfg["n_layers"])
+        torch.cuda.synchronize()
+        self.cache64 = OT.populate(to_f64(self.xp), self.w64, cfg, cfg["n_layers"])
+
+
+@pytest.fixture(scope="module", params=range(len(SMALL)), ids=["gqa64", "mha128", "g7n1"])
+def setup(request):
+    s = Setup(SMALL[request.param])
+    yield s
+    s.model.close()
+
+
+def test_populate_cache_contents(setup):
+    s = setup
+    cfg, m = s.cfg, s.spec["m"]
+    L, Hkv, dh, h = cfg["n_layers"], cfg["n_kv_heads"], cfg["head_dim"], cfg["hidden"]
+    mem = s.model.cache_tensor(s.key).cpu()
+    kv_bytes = L * 2 * Hkv * m * dh * 2
+    kv = mem[:kv_bytes].view(torch.bfloat16).view(L, 2, Hkv, m, dh).float().double().numpy()
+    h_off = s.model.cache_offset(m, L, 0, 2, 0, 0, 0)
+    H = mem[h_off:h_off + L * m * h * 4].view(torch.float32).view(L, m, h).double().numpy()
+    # H$[0] is the exact widening of the prefix input: bit-exact
+    np.testing.assert_array_equal(H[0], to_f64(s.xp))
+    # KV$ is stored in bf16 (values up to ~5, where one bf16 ulp is 2^-5):
+    # checked with the bf16 storage tolerance; H$ is fp32 and checked directly.
+    for l in range(L):
+        assert_close_bf16_store(kv[l, 0], s.cache64["k"][l], f"KV$ K layer {l}")
+        assert_close_bf16_store(kv[l, 1], s.cache64["v"][l], f"KV$ V layer {l}")
+        assert_close(H[l], s.cache64["h"][l], f"H$ layer {l}")
+
+
+def test_step_every_depth(setup):
+    s = setup
+    cfg = s.cfg
+    xs_dev = s.xs.cuda()
+    for d in range(cfg["n_layers"] + 1):
+        say(f"step d={d}")
+        out = torch.full(tuple(s.xs.shape), float("nan"), device="cuda")
+        s.model.step(s.key, xs_dev, d, out=out)
+        torch.cuda.synchronize()
+        ref = OT.step(s.cache64, to_f64(s.xs), d, s.w64, cfg)
+        assert_close(out.cpu().numpy(), ref, f"step d={d}")
+
+
+def test_step_plan_matches_launch_shape(setup):
+    s = setup
+    L = s.cfg["n_layers"]
+    m, B, n_s = s.spec["m"], s.spec["B"], s.spec["n_s"]
+    rows, pos, kv, rh = s.model.step_plan(m, B, n_s, 1)
+    assert rows == [B * n_s] + [B * (m + n_s)] * (L - 1)
+    assert pos == [m] + [0] * (L - 1) and kv == [1] + [0] * (L - 1) and rh == (1 if L > 1 else -1)
+
+
+def test_step_is_deterministic(setup):
+    s = setup
+    xs_dev = s.xs.cuda()
+    a = s.model.step(s.key, xs_dev, 1).clone()
+    b = s.model.step(s.key, xs_dev, 1)
+    torch.cuda.synchronize()
+    assert torch.equal(a, b)
+
+
+def test_requests_independent_on_gpu(setup):
+    s = setup
+    B = s.spec["B"]
+    xs_dev = s.xs.cuda()
+    full = s.model.step(s.key, xs_dev, 1).clone()
+    perm = list(reversed(range(B)))
+    permuted = s.model.step(s.key, xs_dev[perm].contiguous(), 1)
+    one = s.model.step(s.key, xs_dev[:1].contiguous(), 1)
+    torch.cuda.synchronize()
+    assert torch.equal(permuted, full[perm])
+    # a different batch size changes only how rows are grouped into tiles
+    assert_close(one.cpu().numpy(), full[:1].cpu().numpy(), "B=1 vs batch", 1e-4, 1e-5)
+
+
+def test_store_fifo_invalidate_and_errors():
+    cfg = synth.model_config(n_layers=2, hidden=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn=256)
+    w = [{k: v.cuda() for k, v in lw.items()} for lw in synth.model_weights(cfg, 77)]
+    model = bc.Model(cfg, w, cache_capacity=2)
+    ref = FifoTable(2)
+    xp = synth.gaussian((40, 256), 1).cuda()
+    xs = synth.gaussian((2, 8, 256), 2).cuda()
+    for key in (101, 202, 303, 202, 404, 505):
+        say(f"populate key {key}")
+        if key in ref.entries:
+            with pytest.raises(bc.BiCacheError) as ei:
+                model.populate(key, xp, 2)
+            assert ei.value.status == -5
+            continue
+        ev = model.populate(key, xp, 2)
+        assert ev == ref.insert(key, None)
+        assert model.cache_keys() == ref.order()
+    torch.cuda.synchronize()
+    assert model.lookup(505) == (40, 2) and model.lookup(101) is None
+    model.invalidate(505)
+    ref.invalidate(505)
+    assert model.cache_keys() == ref.order() == [404]
+    with pytest.raises(bc.BiCacheError) as ei:
+        model.step(505, xs, 1)
+    assert ei.value.status == -2
+    out = model.step(404, xs, 2)
+    with pytest.raises(bc.BiCacheError) as ei:        # d beyond the cached layers
+        model.populate(606, xp, 1)
+        model.step(606, xs, 2)
+    assert ei.value.status == -1
+    torch.cuda.synchronize()
+    assert torch.isfinite(out).all()
+    model.close()
