@@ -1,0 +1,268 @@
+#!/usr/bin/env python3
+"""Benchmark of the BiCache shared-prefix denoising step on one MI355X.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--depth d]
+
+Workload (one "step" = one bc_step_forward call, the whole hot path):
+  32-layer random-init transformer of the LLaDA-8B layer shape (hidden 4096,
+  32 x 128 heads, SwiGLU 12288, RMSNorm, RoPE), bf16 weights and operands,
+  fp32 residual; B = 16 requests sharing a cached 1536-token prefix, each with
+  512 suffix tokens (shared-prefix ratio 0.75), reuse depth d (default 8):
+  layers 0..d-1 project only the suffix rows and attend over the cached prefix
+  K/V; layers d..31 recompute the prefix with full bidirectional attention.
+  Inputs are seeded synthetic Gaussians already resident in HBM.
+
+Prints ONE JSON line: request-denoise-steps/s of that step (value), the
+roofline of its dominant kernel (the gate/up + SwiGLU GEMM) measured live with
+HIP events inside the timed region, the fp64 CPU oracle timed on a bounded
+sample (rank 0), plus the per-depth step times and the shared-prefix attention
+throughput of the attention-only workloads.
+"""
+import argparse
+import json
+import math
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "request-denoise-steps/s + shared-prefix attn TFLOP/s (% MFMA peak), LLaDA-8B shape"
+PEAK_BF16_TFLOPS = 2516.6      # MI355X dense bf16 MFMA
+PEAK_HBM_GBS = 8000.0
+
+
+def step_flops(cfg, B, m, n_s, d):
+    """Algorithmic FLOPs of one step: linear layers 2*(rows)*(params) and
+    attention 4*n_q*n_k*dh per (request, head), no causal halving."""
+    h, F, L = cfg["hidden"], cfg["ffn"], cfg["n_layers"]
+    Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
+    lin = 2 * (h * (Hq + 2 * Hkv) * dh + Hq * dh * h + 3 * h * F)
+    N = m + n_s
+    shallow = B * n_s * lin + 4 * B * Hq * n_s * N * dh
+    deep = B * N * lin + 4 * B * Hq * N * N * dh
+    return d * shallow + (L - d) * deep
+
+
+def gate_up_flops(cfg, rows):
+    return 2.0 * rows * 2 * cfg["ffn"] * cfg["hidden"]
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__.split("\n")[1])
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--depth", type=int, default=8)
+    ap.add_argument("--depth-steps", type=int, default=3, help="timed steps per extra depth")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    args = ap.parse_args()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures the single-GPU path only (asked for --gpus {args.gpus}, "
+              f"WORLD_SIZE={world}); multi-GPU sharding is described in DESIGN.md, not run.",
+              file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2606_07571_amd as bc
+    from paper_2606_07571_amd import synth
+
+    bc.lib()                                   # fails loudly if the library is not built
+    dev = torch.device("cuda", 0)
+    torch.cuda.set_device(dev)
+    log = lambda *a: print(*a, file=sys.stderr, flush=True)
+
+    # ---------------------------------------------------------------- C3 setup
+    cfg = synth.model_config()
+    sc = synth.STEP_CONFIG
+    B, m, n_s, d = sc["B"], sc["m"], sc["n_s"], args.depth
+    L = cfg["n_layers"]
+    log(f"bench: generating 32-layer weights on the device ({cfg})")
+    weights = synth.model_weights(cfg, 3000, device=dev)
+    xp, xs = synth.step_inputs(cfg, B, m, n_s, 3500, device=dev)
+    model = bc.Model(cfg, weights, cache_capacity=4)
+    key = bc.prefix_key(range(m))
+    model.populate(key, xp, L)
+    torch.cuda.synchronize()
+    out = torch.empty((B, n_s, cfg["hidden"]), dtype=torch.float32, device=dev)
+
+    # populate timing (prefix-only forward of all 32 layers, m = 1536)
+    model.invalidate(key)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    model.populate(key, xp, L)
+    torch.cuda.synchronize()
+    populate_ms = (time.perf_counter() - t0) * 1e3
+
+    # ---------------------------------------------------------------- timed steps
+    log(f"bench: warmup {args.warmup}, timed {args.steps} steps at d={d}")
+    for _ in range(args.warmup):
+        model.step(key, xs, d, out=out)
+    torch.cuda.synchronize()
+    ev0, ev1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    model.profile_begin(["gate_up_swiglu"])    # HIP events around the dominant kernel only
+    torch.cuda.synchronize()
+    w0 = time.perf_counter()
+    ev0.record()
+    for _ in range(args.steps):
+        model.step(key, xs, d, out=out)
+    ev1.record()
+    torch.cuda.synchronize()
+    wall_ms = (time.perf_counter() - w0) * 1e3
+    prof = model.profile_end()
+    ms_per_step = ev0.elapsed_time(ev1) / args.steps
+    value = B / (ms_per_step / 1e3)
+
+    gu_ms, gu_n = prof["gate_up_swiglu"]
+    rows_per_step = d * B * n_s + (L - d) * B * (m + n_s)
+    gu_flops = gate_up_flops(cfg, rows_per_step) * args.steps
+    gu_tflops = gu_flops / (gu_ms / 1e3) / 1e12
+    roofline = {"bound": "mfma", "kernel": "gate_up_swiglu GEMM (bf16 MFMA)",
+                "achieved": round(gu_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
+                "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "launches": gu_n, "avg_launch_ms": round(gu_ms / gu_n, 4)}
+
+    # per-kernel breakdown of one extra profiled step (all classes)
+    model.profile_begin()
+    model.step(key, xs, d, out=out)
+    breakdown = {k: round(v[0], 3) for k, v in model.profile_end().items()}
+
+    # ---------------------------------------------------------------- other depths
+    per_depth = {}
+    for dd in sorted(set([0, 4, 8, 16, d])):
+        model.step(key, xs, dd, out=out)
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(args.depth_steps):
+            model.step(key, xs, dd, out=out)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / args.depth_steps
+        per_depth[dd] = {"ms": round(t, 3), "request_steps_per_s": round(B / (t / 1e3), 2),
+                         "tflops": round(step_flops(cfg, B, m, n_s, dd) / (t / 1e3) / 1e12, 1)}
+    base = per_depth[0]["ms"]
+    f0 = step_flops(cfg, B, m, n_s, 0)
+    for dd, r in per_depth.items():
+        r["speedup_vs_d0"] = round(base / r["ms"], 3)
+        r["ideal_speedup"] = round(f0 / step_flops(cfg, B, m, n_s, dd), 3)
+
+    # C4 populate: 8 layers of the same shape over an 8192-token prefix
+    xp4 = synth.gaussian((8192, cfg["hidden"]), 4100, device=dev)
+    key4 = bc.prefix_key(range(8192))
+    model.populate(key4, xp4, 8)
+    model.invalidate(key4)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    model.populate(key4, xp4, 8)
+    torch.cuda.synchronize()
+    pop4_ms = (time.perf_counter() - t0) * 1e3
+    model.invalidate(key4)
+    del xp4
+    model.close()
+    del weights, model
+    torch.cuda.empty_cache()
+
+    # ---------------------------------------------------------------- attention configs
+    attention = {}
+    for cid in (0, 1, 2, 4):
+        s = synth.ATTN_CONFIGS[cid]
+        ins = synth.attention_inputs(s, 1000 * cid, device=dev)
+        o = torch.empty((s.B, s.Hq, s.n_s, s.dh), dtype=torch.float32, device=dev)
+        for _ in range(3):
+            bc.shared_prefix_attention(*ins, out=o)
+        torch.cuda.synchronize()
+        n = 20
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            bc.shared_prefix_attention(*ins, out=o)
+        e1.record()
+        torch.cuda.synchronize()
+        t = e0.elapsed_time(e1) / n
+        fl = 4.0 * s.B * s.Hq * s.n_s * (s.m + s.n_s) * s.dh
+        attention[f"C{cid}"] = {"ms": round(t, 4), "tflops": round(fl / (t / 1e3) / 1e12, 1),
+                                "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        del ins, o
+
+    # ---------------------------------------------------------------- CPU oracle baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(cfg, B, m, n_s, d, log)
+
+    line = {
+        "metric": METRIC,
+        "value": round(value, 3),
+        "unit": "request-steps/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_per_step, 3),
+        "wall_ms_per_step": round(wall_ms / args.steps, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic (seeded Gaussian inputs, random-init weights)",
+        "config": {"workload": f"full 32-layer denoising step, LLaDA-8B layer shape (h=4096, 32x128 heads, "
+                               f"SwiGLU 12288), B={B} requests, shared prefix {m} + suffix {n_s} tokens, "
+                               f"reuse depth d={d}",
+                   "global_batch": B, "seq_len": m + n_s, "prefix": m, "suffix": n_s, "depth": d,
+                   "parallelism": "single GPU"},
+        "step_tflops": round(step_flops(cfg, B, m, n_s, d) / (ms_per_step / 1e3) / 1e12, 1),
+        "roofline": roofline,
+        "cpu_baseline": cpu,
+        "per_depth": per_depth,
+        "kernel_ms_one_step": breakdown,
+        "attention": attention,
+        "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(cfg, B, m, n_s, d, log, n_req=6):
+    """The fp64 oracle on a bounded sample of the same step: requests 0..n_req-1,
+    each through one shallow layer (its suffix rows over [cached prefix ;
+    suffix]) and one deep layer (all m + n_s rows), at full width.  The step
+    time of one request is extrapolated as d * t_shallow + (L - d) * t_deep
+    (every layer of a kind costs the same) and reported in the metric's unit."""
+    import numpy as np
+    import torch
+    from oracle import transformer as OT
+    from paper_2606_07571_amd import synth
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([p.get("num_threads", 1) for p in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count()
+    log("bench: timing the fp64 oracle sample on the host")
+    w = [{k: synth.to_f64(v) for k, v in synth.layer_weights(cfg, l, 3000, device="cuda").items()}
+         for l in (0, 1)]
+    xp, xs = synth.step_inputs(cfg, B, m, n_s, 3500, device="cuda")
+    xp, xs = synth.to_f64(xp), synth.to_f64(xs[:n_req])
+    torch.cuda.empty_cache()
+    # prefix K/V of layer 0 (what populate would have cached), not timed
+    _, kp, vp = OT.project_qkv(xp, w[0], cfg, np.arange(m))
+    t_sh = t_dp = 0.0
+    for b in range(n_req):
+        t0 = time.perf_counter()
+        OT.layer_suffix(xs[b], w[0], cfg, kp, vp, m + np.arange(n_s))
+        t_sh += time.perf_counter() - t0
+        t0 = time.perf_counter()
+        OT.layer_full(np.concatenate([xp, xs[b]]), w[1], cfg, np.arange(m + n_s))
+        t_dp += time.perf_counter() - t0
+    t_sh, t_dp = t_sh / n_req, t_dp / n_req
+    L = cfg["n_layers"]
+    t_req = d * t_sh + (L - d) * t_dp
+    return {"value": round(1.0 / t_req, 6), "unit": "request-steps/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"requests 0..{n_req - 1} of {B}, each through one shallow layer (mean {t_sh:.2f} s) "
+                      f"and one deep layer (mean {t_dp:.2f} s) at full width; one request-step "
+                      f"extrapolated as {d} shallow + {L - d} deep layers",
+            "sample_seconds": round(n_req * (t_sh + t_dp), 2)}
+
+
+if __name__ == "__main__":
+    main()

@@ -58,7 +58,13 @@ _SIGS = {
     "bc_step_forward": (C.c_int, [C.c_void_p, C.c_uint64, C.c_void_p, C.c_int, C.c_int, C.c_int,
                                   C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_shared_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
+    "bc_profile_begin": (C.c_int, [C.c_void_p, C.c_uint]),
+    "bc_profile_end": (C.c_int, [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int)]),
 }
+
+# kernel classes of bc_profile_* (include/bicache.h)
+KERNEL_CLASSES = ("rmsnorm", "qkv_rope", "attn_shared", "attn_full", "o_proj", "gate_up_swiglu",
+                  "down", "other")
 
 _lib = None
 
@@ -217,6 +223,21 @@ class Model:
 
     def cache_tensor(self, key):
         return self._entries[key]
+
+    # ---------------------------------------------------------------- profiling
+    def profile_begin(self, classes=KERNEL_CLASSES):
+        """Time every later launch of the named kernel classes with HIP events."""
+        mask = 0
+        for c in classes:
+            mask |= 1 << KERNEL_CLASSES.index(c)
+        _check(lib().bc_profile_begin(self._h, mask))
+
+    def profile_end(self):
+        """Returns {class: (total_ms, launches)} of the timed launches."""
+        n = len(KERNEL_CLASSES)
+        ms, cnt = (C.c_double * n)(), (C.c_int * n)()
+        _check(lib().bc_profile_end(self._h, ms, cnt))
+        return {KERNEL_CLASSES[i]: (ms[i], cnt[i]) for i in range(n) if cnt[i]}
 
     # ---------------------------------------------------------------- step
     def step_workspace_bytes(self, m, B, n_s, d):
