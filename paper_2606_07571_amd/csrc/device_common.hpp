@@ -55,6 +55,17 @@ __device__ __forceinline__ int xcd_remap(int bid, int n) {
   return x * q + (x < r ? x : r) + k;
 }
 
+// v_permlane32_swap(x, x) returns, in every lane l, the pair {x[l], x[l ^ 32]}
+// (in some order), so the max / sum over lanes l and l ^ 32 needs no LDS.
+__device__ __forceinline__ float half_max(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return fmaxf(__uint_as_float(r[0]), __uint_as_float(r[1]));
+}
+__device__ __forceinline__ float half_sum(float v) {
+  const auto r = __builtin_amdgcn_permlane32_swap(__float_as_uint(v), __float_as_uint(v), false, false);
+  return __uint_as_float(r[0]) + __uint_as_float(r[1]);
+}
+
 __device__ __forceinline__ float wave_sum(float v) {
 #pragma unroll
   for (int o = 32; o >= 1; o >>= 1) v += __shfl_xor(v, o, kWave);

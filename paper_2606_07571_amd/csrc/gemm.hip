@@ -10,12 +10,11 @@
 // Tiling: a workgroup computes a BM x BN tile with WM x WN waves; each wave
 // owns a (BM/WM) x (BN/WN) sub-tile made of 32x32 MFMA blocks
 // (v_mfma_f32_32x32x16_bf16).  K advances in steps of 64 through a
-// double-buffered LDS ring: the next step's A/B tiles are fetched from global
-// memory into registers while the current step's MFMAs run, then written to
-// the other LDS buffer, with one barrier per step.  LDS rows are 128 bytes
-// (64 bf16); the 16-byte chunk index is XOR-swizzled with the row's low 3 bits
-// so that the 8 lanes served together by a 128-bit LDS access always touch 8
-// different bank groups, for both the fills and the fragment reads.
+// double-buffered LDS ring fed through registers: step k+1's tiles are written
+// to the other LDS buffer halfway through step k's MFMAs and step k+2's global
+// loads are issued right after, with one barrier per step.  LDS rows are 128 bytes
+// (64 bf16) with an XOR-swizzled 16-byte chunk index (see swz), conflict-free
+// for both the fills and the fragment reads.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -34,7 +33,11 @@ struct GemmArgs {
   int M, K;
 };
 
-__device__ __forceinline__ int swz(int row, int kc) { return row * BK + ((kc ^ (row & 7)) << 3); }
+// LDS serves 128-bit accesses 16 lanes (256 bytes, 64 banks) at a time; with
+// 128-byte rows two consecutive rows fill the 64 banks, so the chunk index is
+// XOR-ed with (row >> 1) & 7: the 16 rows read together by a fragment load, and
+// the 2 rows x 8 chunks written together by a fill, all land on distinct banks.
+__device__ __forceinline__ int swz(int row, int kc) { return row * BK + ((kc ^ ((row >> 1) & 7)) << 3); }
 
 // ---------------------------------------------------------------- epilogues
 // Each epilogue says how many BN-wide tiles cover its output (tiles_n), which
@@ -223,24 +226,26 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
 
   u32x4 ra[A_PER], rb[B_PER];
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  // Loads are unconditional (an invalid row reads the clamped row 0, always in
+  // bounds) so that no load sits behind a divergent branch; rows outside the
+  // matrix are zeroed only when the registers are written to LDS, after the
+  // current step's MFMAs, so the load latency stays hidden behind them.
   auto fetch = [&](int k0) {
 #pragma unroll
-    for (int p = 0; p < A_PER; ++p)
-      ra[p] = a_ok[p] ? *reinterpret_cast<const u32x4*>(a_src[p] + k0) : zero4;
+    for (int p = 0; p < A_PER; ++p) ra[p] = *reinterpret_cast<const u32x4*>(a_src[p] + k0);
 #pragma unroll
-    for (int p = 0; p < B_PER; ++p)
-      rb[p] = b_ok[p] ? *reinterpret_cast<const u32x4*>(b_src[p] + k0) : zero4;
+    for (int p = 0; p < B_PER; ++p) rb[p] = *reinterpret_cast<const u32x4*>(b_src[p] + k0);
   };
   auto stash = [&](int buf) {
 #pragma unroll
     for (int p = 0; p < A_PER; ++p) {
       const int r = (tid >> 3) + p * (NT / 8);
-      *reinterpret_cast<u32x4*>(&sA[buf][swz(r, kc)]) = ra[p];
+      *reinterpret_cast<u32x4*>(&sA[buf][swz(r, kc)]) = a_ok[p] ? ra[p] : zero4;
     }
 #pragma unroll
     for (int p = 0; p < B_PER; ++p) {
       const int r = (tid >> 3) + p * (NT / 8);
-      *reinterpret_cast<u32x4*>(&sB[buf][swz(r, kc)]) = rb[p];
+      *reinterpret_cast<u32x4*>(&sB[buf][swz(r, kc)]) = b_ok[p] ? rb[p] : zero4;
     }
   };
 
@@ -251,15 +256,9 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
     for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
 
   const int ksteps = a.K / BK;
-  fetch(0);
-  stash(0);
-  __syncthreads();
-
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int cur = ks & 1;
-    if (ks + 1 < ksteps) fetch((ks + 1) * BK);
+  auto compute = [&](int cur, int kk0, int kk1) {
 #pragma unroll
-    for (int kk = 0; kk < BK / 16; ++kk) {
+    for (int kk = kk0; kk < kk1; ++kk) {
       const int kci = kk * 2 + (lane >> 5);
       bf16x8 af[FM], bfr[FN];
 #pragma unroll
@@ -277,7 +276,26 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
 #pragma unroll
         for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(af[i], bfr[j], acc[i][j]);
     }
-    if (ks + 1 < ksteps) stash(cur ^ 1);
+  };
+
+  // Pipeline: the registers hold step ks+1 while step ks computes; they are
+  // written to the other LDS buffer halfway through step ks (that buffer was
+  // last read in step ks-1, before the previous barrier), and step ks+2 is
+  // fetched right after, so its loads have a whole step to arrive and the LDS
+  // writes overlap the second half of the step's MFMAs.
+  fetch(0);
+  stash(0);
+  if (ksteps > 1) fetch(BK);
+  __syncthreads();
+
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int cur = ks & 1;
+    compute(cur, 0, BK / 32);
+    if (ks + 1 < ksteps) {
+      stash(cur ^ 1);
+      if (ks + 2 < ksteps) fetch((ks + 2) * BK);
+    }
+    compute(cur, BK / 32, BK / 16);
     __syncthreads();
   }
 
