@@ -8,7 +8,9 @@ tests/native/libbicache_table_host.so (the FIFO table and the prefix-key hash
 compiled with the system C++ compiler, no HIP) used by the CPU tests.
 """
 import concurrent.futures as cf
+import json
 import os
+import re
 import shutil
 import subprocess
 import sys
@@ -32,14 +34,40 @@ FLAGS = [
 ]
 
 
+RESOURCES = os.path.join(BUILD, "kernel_resources.json")
+
+
+def _parse_resources(stderr):
+    """Per-kernel VGPR/AGPR/scratch/spill/LDS figures from the compiler's
+    kernel-resource-usage remarks."""
+    out, cur = {}, None
+    for line in stderr.splitlines():
+        m = re.search(r"remark: (.*?) \[-Rpass-analysis=kernel-resource-usage\]", line)
+        if not m:
+            continue
+        t = m.group(1).strip()
+        if t.startswith("Function Name:"):
+            cur = t.split(":", 1)[1].strip()
+            out[cur] = {}
+        elif cur and ":" in t:
+            k, v = t.split(":", 1)
+            try:
+                out[cur][k.strip()] = int(v.strip())
+            except ValueError:
+                out[cur][k.strip()] = v.strip()
+    return out
+
+
 def _compile(src):
     obj = os.path.join(BUILD, os.path.basename(src) + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+    extra = ["-Rpass-analysis=kernel-resource-usage"] if src.endswith(".hip") else []
+    cmd = [HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", obj]
     r = subprocess.run(cmd, capture_output=True, text=True)
-    err = "\n".join(l for l in r.stderr.splitlines() if "packed-fp32-ops" not in l)
+    err = "\n".join(l for l in r.stderr.splitlines()
+                    if "packed-fp32-ops" not in l and "kernel-resource-usage" not in l)
     if r.returncode != 0:
         raise RuntimeError(f"compiling {src} failed:\n{err}")
-    return obj
+    return obj, _parse_resources(r.stderr)
 
 
 def build_host_lib():
@@ -55,7 +83,13 @@ def build_host_lib():
 def build(verbose=True):
     os.makedirs(BUILD, exist_ok=True)
     with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
-        objs = list(ex.map(_compile, SOURCES))
+        results = list(ex.map(_compile, SOURCES))
+    objs = [o for o, _ in results]
+    resources = {}
+    for _, res in results:
+        resources.update(res)
+    with open(RESOURCES, "w") as f:
+        json.dump(resources, f, indent=1, sort_keys=True)
     tmp = LIB + ".tmp"
     cmd = [HIPCC, f"--offload-arch={ARCH}", "-shared", "-fPIC", *objs, "-o", tmp]
     r = subprocess.run(cmd, capture_output=True, text=True)

@@ -119,7 +119,7 @@ __global__ void __launch_bounds__(NW * kWave)
   const int n_tiles = TP + (b_hi - b_lo + 1) * TS;
 
   // tile t -> (K rows, V rows, row stride, valid keys, owning request or -1)
-  auto tile_src = [&](int t, const bf16*& kb, const bf16*& vb, long& rs, int& nv, int& owner) {
+  auto tile_src = [&](int t, const bf16*& kb, const bf16*& vb, long& rs, int& nv, int& owner) __attribute__((always_inline)) {
     if (t < TP) {
       kb = (const bf16*)a.kp + g * a.p_sh + (long)t * KT * DH;
       vb = (const bf16*)a.vp + g * a.p_sh + (long)t * KT * DH;
@@ -160,7 +160,7 @@ __global__ void __launch_bounds__(NW * kWave)
   u32x4 kreg[K_PER], vreg[V_PER][2];
   int nv_next = 0;
   const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  auto fetch = [&](int t) {
+  auto fetch = [&](int t) __attribute__((always_inline)) {
     const bf16 *kb, *vb;
     long rs;
     int owner;
@@ -191,7 +191,7 @@ __global__ void __launch_bounds__(NW * kWave)
       }
     }
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf) __attribute__((always_inline)) {
     if (nv_next < KT) {  // partial tile: zero the rows past the valid keys
 #pragma unroll
       for (int p = 0; p < K_PER; ++p) {

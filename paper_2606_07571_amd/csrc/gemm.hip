@@ -45,17 +45,36 @@ __device__ __forceinline__ int swz(int row, int kc) { return row * BK + ((kc ^ (
 // accumulators are written (apply).  Accumulator (i, j, e) of lane l holds
 // C[row0 + i*32 + 8*(e/4) + 4*(l/32) + e%4][col0 + j*32 + l%32].
 
+// R += A . W^T: the accumulators start from the residual tile (init), so the
+// residual is read while the first K steps load and the epilogue only writes.
 struct EpiResidual {
   float* R;
   int ldr, N;
+  static constexpr bool kInit = true;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(N, BN); }
   template <int BN, int TN>
-  __device__ int w_row(int tn, int r) const {
+  __device__ __forceinline__ int w_row(int tn, int r) const {
     int n = tn * BN + r;
     return n < N ? n : -1;
   }
   template <int BN, int TN, int FM, int FN>
-  __device__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
+  __device__ __forceinline__ void init(f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn, int lane) const {
+    const int col0 = tn * BN + wn * TN + (lane & 31);
+#pragma unroll
+    for (int i = 0; i < FM; ++i)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int row = row0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+        const float* rp = R + (long)(row < M ? row : 0) * ldr;
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          const int col = col0 + j * 32;
+          acc[i][j][e] = (row < M && col < N) ? rp[col] : 0.f;
+        }
+      }
+  }
+  template <int BN, int TN, int FM, int FN>
+  __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
                         int lane) const {
     const int col0 = tn * BN + wn * TN + (lane & 31);
 #pragma unroll
@@ -68,7 +87,7 @@ struct EpiResidual {
 #pragma unroll
         for (int j = 0; j < FN; ++j) {
           const int col = col0 + j * 32;
-          if (col < N) rp[col] += acc[i][j][e];
+          if (col < N) rp[col] = acc[i][j][e];
         }
       }
   }
@@ -80,16 +99,17 @@ struct EpiResidual {
 struct EpiSwiGLU {
   bf16* act;
   int F;
+  static constexpr bool kInit = false;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(F, BN / 2); }
   template <int BN, int TN>
-  __device__ int w_row(int tn, int r) const {
+  __device__ __forceinline__ int w_row(int tn, int r) const {
     const int wn = r / TN, q = r % TN;
     const int half = q / (TN / 2), within = q % (TN / 2);
     const int col = tn * (BN / 2) + wn * (TN / 2) + within;
     return col < F ? half * F + col : -1;
   }
   template <int BN, int TN, int FM, int FN>
-  __device__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
+  __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
                         int lane) const {
     const int col0 = tn * (BN / 2) + wn * (TN / 2) + (lane & 31);
 #pragma unroll
@@ -112,6 +132,7 @@ struct EpiSwiGLU {
 
 template <int DH>
 struct EpiQKV {
+  static constexpr bool kInit = false;
   bf16* q;
   bf16* k;
   bf16* v;
@@ -122,12 +143,12 @@ struct EpiQKV {
   __host__ __device__ int ncols() const { return (Hq + 2 * Hkv) * DH; }
   __host__ __device__ int tiles_n(int BN) const { return cdiv(ncols(), BN); }
   template <int BN, int TN>
-  __device__ int w_row(int tn, int r) const {
+  __device__ __forceinline__ int w_row(int tn, int r) const {
     int n = tn * BN + r;
     return n < ncols() ? n : -1;
   }
   template <int BN, int TN, int FM, int FN>
-  __device__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
+  __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
                         int lane) const {
     static_assert(TN % DH == 0, "a wave sub-tile must hold whole heads");
     constexpr int BPH = DH / 32;  // 32-column blocks per head
@@ -230,13 +251,13 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
   // bounds) so that no load sits behind a divergent branch; rows outside the
   // matrix are zeroed only when the registers are written to LDS, after the
   // current step's MFMAs, so the load latency stays hidden behind them.
-  auto fetch = [&](int k0) {
+  auto fetch = [&](int k0) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < A_PER; ++p) ra[p] = *reinterpret_cast<const u32x4*>(a_src[p] + k0);
 #pragma unroll
     for (int p = 0; p < B_PER; ++p) rb[p] = *reinterpret_cast<const u32x4*>(b_src[p] + k0);
   };
-  auto stash = [&](int buf) {
+  auto stash = [&](int buf) __attribute__((always_inline)) {
 #pragma unroll
     for (int p = 0; p < A_PER; ++p) {
       const int r = (tid >> 3) + p * (NT / 8);
@@ -255,8 +276,9 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
 
+  if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
   const int ksteps = a.K / BK;
-  auto compute = [&](int cur, int kk0, int kk1) {
+  auto compute = [&](int cur, int kk0, int kk1) __attribute__((always_inline)) {
 #pragma unroll
     for (int kk = kk0; kk < kk1; ++kk) {
       const int kci = kk * 2 + (lane >> 5);
@@ -302,16 +324,156 @@ __global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi e
   epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
 }
 
+// ---------------------------------------------------------------- ping-pong kernel
+// Same 256 x 256 tile and 64 x 128 wave sub-tiles, but the two waves that
+// share a SIMD never do the same kind of work at the same time.  Waves 0-3
+// (group 0, columns 0-127 of the tile) and waves 4-7 (group 1, columns
+// 128-255) run the same program, group 1 one barrier-phase behind.  Each half
+// K step (32 of K) is a memory phase -- read this half step's fragments from
+// LDS, and in the second half also write the next K step's tile to LDS and
+// issue the global loads of the one after it -- then a compute phase of 16
+// MFMAs, with a workgroup barrier between phases.  While one group issues its
+// MFMAs the other group's LDS and global traffic runs, so the matrix pipe of
+// every SIMD is fed alternately by its two waves.
+//
+// LDS tiles are double-buffered: K step k+1 is written during the second half
+// of step k (after every wave has finished reading that buffer's previous
+// tile, step k-1, one phase earlier for group 1) and is first read at step
+// k+1.  Group 0 fetches and writes the A tile, group 1 the W tile, 8 chunks of
+// 16 bytes per lane per K step; each fetch has a whole K step to land.
+template <class Epi>
+__global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
+  constexpr int BM = 256, BN = 256, TM = 64, TN = 128, FM = 2, FN = 4;
+  constexpr int PER = 8;  // 16-byte chunks per lane per K step
+
+  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
+  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int grp = wave >> 2;          // 0: loads A, computes columns 0-127; 1: W, 128-255
+  const int wm = wave & 3, wn = grp;  // the two waves on a SIMD are w and w + 4
+
+  const int tiles_m = cdiv(a.M, BM), tiles_n = epi.tiles_n(BN);
+  const int lid = xcd_remap(blockIdx.x, gridDim.x);
+  constexpr int GM = 8;
+  const int per_group = GM * tiles_n;
+  const int first_m = (lid / per_group) * GM;
+  const int gsz = min(tiles_m - first_m, GM);
+  const int tm = first_m + (lid % per_group) % gsz;
+  const int tn = (lid % per_group) / gsz;
+  const int m0 = tm * BM;
+
+  // this lane's chunks of its group's operand tile: chunk q = lane + 64*wm + 256*p
+  // covers tile row q / 8, 16-byte column chunk q % 8
+  const int kc = lane & 7;
+  const bf16* src[PER];
+  bool ok[PER];
+#pragma unroll
+  for (int p = 0; p < PER; ++p) {
+    const int r = (lane >> 3) + 8 * wm + 32 * p;
+    int gr;
+    if (grp == 0) {
+      gr = m0 + r;
+      ok[p] = gr < a.M;
+      src[p] = a.A + (long)(ok[p] ? gr : 0) * a.lda + kc * 8;
+    } else {
+      gr = epi.template w_row<BN, TN>(tn, r);
+      ok[p] = gr >= 0;
+      src[p] = a.W + (long)(ok[p] ? gr : 0) * a.ldw + kc * 8;
+    }
+  }
+  bf16* const dst0 = grp == 0 ? &sA[0][0] : &sB[0][0];
+  u32x4 stage[PER];
+  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  auto fetch = [&](int k0) __attribute__((always_inline)) {
+#pragma unroll
+    for (int p = 0; p < PER; ++p) stage[p] = *reinterpret_cast<const u32x4*>(src[p] + k0);
+  };
+  auto stash = [&](int buf) __attribute__((always_inline)) {
+    bf16* dst = dst0 + buf * (BM * BK);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int r = (lane >> 3) + 8 * wm + 32 * p;
+      *reinterpret_cast<u32x4*>(&dst[swz(r, kc)]) = ok[p] ? stage[p] : zero4;
+    }
+  };
+
+  f32x16 acc[FM][FN];
+#pragma unroll
+  for (int i = 0; i < FM; ++i)
+#pragma unroll
+    for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
+
+  bf16x8 fa[2][FM], fb[2][FN];
+  auto init_acc = [&]() __attribute__((always_inline)) {
+    if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
+  };
+  auto read_frags = [&](int cur, int h) __attribute__((always_inline)) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2) {
+      const int kci = (2 * h + k2) * 2 + (lane >> 5);
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+        fa[k2][i] = *reinterpret_cast<const bf16x8*>(&sA[cur][swz(wm * TM + i * 32 + (lane & 31), kci)]);
+#pragma unroll
+      for (int j = 0; j < FN; ++j)
+        fb[k2][j] = *reinterpret_cast<const bf16x8*>(&sB[cur][swz(wn * TN + j * 32 + (lane & 31), kci)]);
+    }
+  };
+  auto mma = [&]() __attribute__((always_inline)) {
+#pragma unroll
+    for (int k2 = 0; k2 < 2; ++k2)
+#pragma unroll
+      for (int i = 0; i < FM; ++i)
+#pragma unroll
+        for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(fa[k2][i], fb[k2][j], acc[i][j]);
+  };
+
+  // A phase boundary: the workgroup barrier, fenced so that the compiler
+  // cannot move MFMAs (which touch no memory) across it.
+  auto phase = []() __attribute__((always_inline)) {
+    __builtin_amdgcn_sched_barrier(0);
+    __syncthreads();
+    __builtin_amdgcn_sched_barrier(0);
+  };
+
+  const int ksteps = a.K / BK;
+  fetch(0);
+  init_acc();  // its loads overlap the first tile's
+  stash(0);
+  if (ksteps > 1) fetch(BK);
+  phase();
+  if (grp == 1) phase();  // group 1 runs one phase behind
+
+  for (int ks = 0; ks < ksteps; ++ks) {
+    const int cur = ks & 1;
+    read_frags(cur, 0);
+    phase();
+    mma();
+    phase();
+    read_frags(cur, 1);
+    if (ks + 1 < ksteps) {
+      stash(cur ^ 1);
+      if (ks + 2 < ksteps) fetch((ks + 2) * BK);
+    }
+    phase();
+    mma();
+    phase();
+  }
+  if (grp == 0) phase();  // match group 1's extra barrier
+
+  epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
+}
+
 // 256 x 256 tiles, 8 waves as 4 (M) x 2 (N): 64 x 128 per wave, so a wave's
 // columns span whole 128-wide heads (RoPE pairs stay lane-local).
 constexpr int kBM = 256, kBN = 256, kWM = 4, kWN = 2;
 
 template <class Epi>
 hipError_t launch(const GemmArgs& a, const Epi& epi, hipStream_t s) {
-  const int tiles = cdiv(a.M, kBM) * epi.tiles_n(kBN);
+  const int tiles = cdiv(a.M, 256) * epi.tiles_n(256);
   if (tiles == 0) return hipSuccess;
-  hipLaunchKernelGGL((gemm_kernel<kBM, kBN, kWM, kWN, Epi>), dim3(tiles), dim3(kWM * kWN * kWave),
-                     0, s, a, epi);
+  hipLaunchKernelGGL((gemm_pp_kernel<Epi>), dim3(tiles), dim3(512), 0, s, a, epi);
   return hipGetLastError();
 }
 
