@@ -3,16 +3,14 @@
 // the deep layers' full attention of every request over its own sequence.
 //
 // Work decomposition.  For one KV head g, the query rows of every request b
-// and every query head of g's group are cut into chunks of QB*32 rows
-// (b, head, i0); a workgroup of NW waves takes NW consecutive chunks, one per
-// wave.  A wave holds QB query blocks of 32 rows, so every K or V fragment it
-// reads from LDS feeds QB MFMAs.  The key
-// sequence the workgroup walks is
+// and every query head of g's group are cut into chunks of 32 rows
+// (b, head, i0); a workgroup of 8 waves takes 8 consecutive chunks, one per
+// wave.  The key sequence the workgroup walks is
 //     [the prefix tiles of g]  then, for each distinct request among its
 //     chunks, [that request's suffix tiles of g],
 // in tiles of 64 keys staged through LDS.  A prefix tile is loaded once per
-// workgroup and consumed by all NW waves, whatever request or query head they
-// serve, so one LDS copy of the shared prefix feeds up to NW*32 query rows of
+// workgroup and consumed by all 8 waves, whatever request or query head they
+// serve, so one LDS copy of the shared prefix feeds up to 256 query rows of
 // several requests.  A suffix tile is consumed only by the waves of its
 // request.
 //
@@ -25,9 +23,39 @@
 // (no data movement; the MFMA's k order is chosen to match the keys a lane
 // already holds) and V^T is read from a transposed LDS copy of the V tile.
 // Softmax runs in fp32 in the log2 domain (exp2 with log2(e) folded into the
-// scale); P is rounded to bf16 for the P.V product.
+// scale); P is rounded to bf16 for the P.V product and the row sum adds the
+// fp32 probabilities.
+//
+// Software pipeline.  Every wave overlaps its own matrix and vector work: in
+// step u it runs
+//   block A: O^T += V(u-1)^T . P(u-1)^T (16 MFMAs) alongside the softmax of
+//            S(u) (row max, running max, P(u) = exp2(...), row sums)
+//   block B: S(u+1)^T = K(u+1) . Q^T (16 MFMAs) alongside this thread's share
+//            of the LDS fill of tile u+2 and the global fetch of tile u+3
+// and one barrier.  The MFMAs of a block do not depend on its vector work, so
+// the two streams issue side by side, and with two such waves per SIMD the
+// vector instructions issue at the SIMD's full rate (one wave alone issues
+// one only every other slot).  The online softmax stays exact: the running
+// max moves (lazily, by more than 8 in log2 units) before P(u) is formed, and
+// O, which holds P(u-1).V(u-1) computed with the old max once block A is
+// done, is rescaled between the blocks.
+//
+// LDS.  Tiles live in a 4-deep ring (tile t in slot t % 4): step u reads
+// V(u-1) and K(u+1) and fills tile u+2, whose slot last held tile u-2.  Rows
+// are padded by 16 bytes (K rows dh+8 elements, V^T rows 72), so the 16 rows
+// that one fragment read touches fall into distinct bank groups and every
+// fragment of a tile sits at a compile-time offset from one per-lane base.
+// In a V^T row the 16 keys of k step s are stored in the order
+// [0-3, 8-11, 4-7, 12-15], which makes the 8 keys lane half h of the P.V MFMA
+// takes (16s + 4h + {0..3} and 16s + 8 + 4h + {0..3}) one 16-byte chunk.
+// Global fetches are buffer loads whose descriptor covers exactly the tile's
+// valid rows, so key rows past the end of a partial tile (and whole tiles past
+// the end of the sequence) read as zero with no masking code.  Key rows of
+// every K/V operand are dh elements apart.
 #include "device_common.hpp"
 #include "kernels.hpp"
+
+#include <type_traits>
 
 namespace bc {
 namespace {
@@ -36,60 +64,33 @@ constexpr int KT = 64;  // keys per LDS tile
 
 __host__ __device__ constexpr int cdiv(int a, int b) { return (a + b - 1) / b; }
 
-// K tile: rows of dh bf16 (KCH 16-byte chunks).  LDS serves 128-bit accesses
-// 16 lanes (256 bytes, 64 banks) at a time, and a fragment read touches 16
-// consecutive rows at one chunk: with 256-byte rows (dh 128) chunk kc of row r
-// is stored at kc ^ (r & 15); with 128-byte rows (dh 64), where two rows share
-// the 64 banks, at kc ^ ((r >> 1) & 7).  Both make those 16 accesses hit
-// distinct banks; a fill writes whole rows, which a permutation keeps
-// conflict-free.
-template <int KCH>
-__device__ __forceinline__ int kofs(int r, int kc) {
-  const int x = KCH == 16 ? (r & 15) : ((r >> 1) & 7);
-  return r * KCH * 8 + ((kc ^ x) << 3);
-}
-
-// V^T tile: row d holds the 64 keys of dim d (128 bytes, 8 chunks of 8 keys).
-// The P.V MFMA of k step s takes, in lane half h, the keys 16s + 4h + {0..3}
-// and 16s + 8 + 4h + {0..3}; storing each 16-key group in the order
-// [0-3, 8-11, 4-7, 12-15] makes those 8 keys one contiguous chunk (2s + h), read
-// with one 128-bit access.  Chunk c of row d lives at chunk c ^ vswz(d).
-__device__ __forceinline__ int vswz(int d) { return (d ^ (d >> 3)) & 7; }
-// element offset (in bf16) of key k of dim d inside the V^T tile
-__device__ __forceinline__ int vofs(int d, int k) {
-  const int s = k >> 4, a = (k >> 2) & 3, i = k & 3;
-  const int chunk = 2 * s + (a & 1), elem = (a >> 1) * 4 + i;
-  return d * KT + ((chunk ^ vswz(d)) << 3) + elem;
-}
-
-template <int DH, int NW, int QB, bool OUT_F32>
-__global__ void __launch_bounds__(NW * kWave)
-    attn_kernel(AttnArgs a, int CQ, int wg_per_group) {
-  constexpr int NT = NW * kWave;
-  constexpr int QR = 32 * QB;                   // query rows per wave
+template <int DH, bool OUT_F32>
+__global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg_per_group) {
+  constexpr int NW = 8, QR = 32;
   constexpr int KCH = DH / 8;                  // 16-byte chunks per key row
-  constexpr int K_PER = KT * KCH / NT;          // K chunks per thread per tile
-  constexpr int VBLK = (KT / 2) * KCH;          // (2 keys x 8 dims) V blocks per tile
-  constexpr int V_PER = (VBLK + NT - 1) / NT;   // ... per thread (the last round may be partial)
-  static_assert(K_PER * NT == KT * KCH, "tile/thread mismatch");
-  constexpr int NB = DH / 32;                   // 32-wide dim blocks of the output
+  constexpr int KROW = DH + 8;                 // K row stride in LDS (elements)
+  constexpr int VROW = KT + 8;                 // V^T row stride in LDS (elements)
+  constexpr int KTILE = KT * KROW, VTILE = DH * VROW, SLOT = KTILE + VTILE;
+  constexpr int NBUF = 4;
+  constexpr int K_PER = KT * KCH / 512;        // 16-byte K chunks per thread per tile
+  constexpr int NB = DH / 32, NKK = DH / 16, NS = KT / 16;
+  constexpr int RSRC_W3 = 0x00020000;          // raw buffer, 32-bit dwords (gfx9 family)
 
-  __shared__ __attribute__((aligned(16))) bf16 Ks[2][KT * DH];
-  __shared__ __attribute__((aligned(16))) bf16 Vt[2][DH * KT];
+  __shared__ __attribute__((aligned(16))) bf16 smem[NBUF * SLOT];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int half = lane >> 5, c = lane & 31;
 
   const int lid = xcd_remap(blockIdx.x, gridDim.x);
   const int g = lid / wg_per_group, wgi = lid % wg_per_group;
   const int G = a.Hq / a.Hkv;
-  const int per_req = G * CQ;                   // chunks per request
+  const int per_req = G * CQ;
   const int total = a.B * per_req;
   const int c0 = wgi * NW;
   const int c_last = min(c0 + NW, total) - 1;
   const int b_lo = c0 / per_req, b_hi = c_last / per_req;
 
-  // this wave's chunk
   const int my = c0 + wave;
   const bool active = my < total;
   const int cc = active ? my : c_last;
@@ -97,310 +98,288 @@ __global__ void __launch_bounds__(NW * kWave)
   const int rem = cc - b * per_req;
   const int hq = g * G + rem / CQ;
   const int i0 = (rem % CQ) * QR;
+  const int qrow = i0 + c;
+  const bool row_ok = active && qrow < a.n_s;
 
-  // Q^T fragments of query block qb: lane supplies Q[row i0 + 32qb + c][dims
-  // 16kk + 8*half .. +8]
-  bf16x8 qf[QB][DH / 16];
-  bool row_ok[QB];
+  bf16x8 qf[NKK];
+  {
+    const bf16* qp = (const bf16*)a.q + b * a.q_sb + hq * a.q_sh + (long)(row_ok ? qrow : 0) * a.q_sr;
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    const int qrow = i0 + 32 * qb + c;
-    row_ok[qb] = active && qrow < a.n_s;
-    const bf16* qp = (const bf16*)a.q + b * a.q_sb + hq * a.q_sh + (long)(row_ok[qb] ? qrow : 0) * a.q_sr;
-#pragma unroll
-    for (int kk = 0; kk < DH / 16; ++kk) {
+    for (int kk = 0; kk < NKK; ++kk) {
       u32x4 v = {0u, 0u, 0u, 0u};
-      if (row_ok[qb]) v = *reinterpret_cast<const u32x4*>(qp + kk * 16 + half * 8);
-      qf[qb][kk] = __builtin_bit_cast(bf16x8, v);
+      if (row_ok) v = *reinterpret_cast<const u32x4*>(qp + kk * 16 + half * 8);
+      qf[kk] = __builtin_bit_cast(bf16x8, v);
     }
   }
 
   const int TP = cdiv(a.m, KT), TS = cdiv(a.n_s, KT);
   const int n_tiles = TP + (b_hi - b_lo + 1) * TS;
-
-  // tile t -> (K rows, V rows, row stride, valid keys, owning request or -1)
-  auto tile_src = [&](int t, const bf16*& kb, const bf16*& vb, long& rs, int& nv, int& owner) __attribute__((always_inline)) {
-    if (t < TP) {
-      kb = (const bf16*)a.kp + g * a.p_sh + (long)t * KT * DH;
-      vb = (const bf16*)a.vp + g * a.p_sh + (long)t * KT * DH;
-      rs = DH;
-      nv = min(KT, a.m - t * KT);
-      owner = -1;
-    } else {
-      const int u = t - TP, rb = b_lo + u / TS, tt = u % TS;
-      const long off = rb * a.s_sb + g * a.s_sh + (long)tt * KT * a.s_sr;
-      kb = (const bf16*)a.ks + off;
-      vb = (const bf16*)a.vs + off;
-      rs = a.s_sr;
-      nv = min(KT, a.n_s - tt * KT);
-      owner = rb;
-    }
+  // a wave works on a tile if it is a prefix tile or a suffix tile of its
+  // own request
+  auto owns = [&](int t) __attribute__((always_inline)) {
+    return active && t >= 0 && t < n_tiles && (t < TP || b_lo + (t - TP) / TS == b);
+  };
+  auto valid_of = [&](int t) __attribute__((always_inline)) {
+    return t < TP ? min(KT, a.m - t * KT) : min(KT, a.n_s - ((t - TP) % TS) * KT);
   };
 
-  // Each thread loads K_PER 16-byte K chunks and V_PER pairs of V rows per
-  // tile.  Its element offsets inside a tile depend only on the row stride
-  // (dh for the prefix, s_sr for a suffix), so they are computed once; a tile
-  // adds its scalar base.  In a partial tile rows past the valid keys re-read
-  // the tile's first row (always in bounds) and are zeroed when stashed.
-  int koff_p[K_PER], koff_s[K_PER], voff_p[V_PER], voff_s[V_PER];
+  // this thread's share of a fill: K chunks q = tid + 512p (row q / KCH,
+  // chunk q % KCH); V key pair kp = tid % 32 of dim group tid / 32
+  int kg_off[K_PER], ks_off[K_PER];
 #pragma unroll
   for (int p = 0; p < K_PER; ++p) {
-    const int q = tid + p * NT, r = q / KCH, kc = q % KCH;
-    koff_p[p] = r * DH + kc * 8;
-    koff_s[p] = r * (int)a.s_sr + kc * 8;
+    const int q = tid + 512 * p, r = q / KCH, kc = q % KCH;
+    kg_off[p] = (r * DH + kc * 8) * 2;                 // bytes from the tile's first row
+    ks_off[p] = r * KROW + kc * 8;                     // elements in the LDS K tile
   }
-#pragma unroll
-  for (int p = 0; p < V_PER; ++p) {
-    const int q = tid + p * NT, dg = q % KCH, kp = q / KCH;
-    const int r0 = q < VBLK ? 2 * kp : 0;
-    voff_p[p] = r0 * DH + dg * 8;
-    voff_s[p] = r0 * (int)a.s_sr + dg * 8;
-  }
+  const int kp = tid & 31, dgl = tid >> 5;
+  const bool v_ok = dgl < KCH;
+  const int dg = v_ok ? dgl : 0;
+  const int vg_off = (2 * kp * DH + dg * 8) * 2;
+  // key 2kp sits at position chunk*8 + elem of its V^T row, with the 16 keys
+  // of step s stored in the order [0-3, 8-11, 4-7, 12-15]
+  const int vpos = ((2 * (kp >> 3) + ((kp >> 1) & 1)) << 3) + ((kp >> 2) & 1) * 4 + 2 * (kp & 1);
+  const int vs_off = KTILE + dg * 8 * VROW + vpos;
 
-  u32x4 kreg[K_PER], vreg[V_PER][2];
-  int nv_next = 0;
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
+  u32x4 kreg[K_PER], vreg[2];
+  // tiles past the end get an empty descriptor: their loads return zeros
   auto fetch = [&](int t) __attribute__((always_inline)) {
-    const bf16 *kb, *vb;
-    long rs;
-    int owner;
-    tile_src(t, kb, vb, rs, nv_next, owner);
-    const bool pre = t < TP;
-    if (nv_next == KT) {
-#pragma unroll
-      for (int p = 0; p < K_PER; ++p)
-        kreg[p] = *reinterpret_cast<const u32x4*>(kb + (pre ? koff_p[p] : koff_s[p]));
-#pragma unroll
-      for (int p = 0; p < V_PER; ++p) {
-        const bf16* vp = vb + (pre ? voff_p[p] : voff_s[p]);
-        vreg[p][0] = *reinterpret_cast<const u32x4*>(vp);
-        vreg[p][1] = *reinterpret_cast<const u32x4*>(vp + rs);
-      }
-    } else {
-#pragma unroll
-      for (int p = 0; p < K_PER; ++p) {
-        const int q = tid + p * NT, r = q / KCH, kc = q % KCH;
-        kreg[p] = *reinterpret_cast<const u32x4*>(kb + (r < nv_next ? r : 0) * rs + kc * 8);
-      }
-#pragma unroll
-      for (int p = 0; p < V_PER; ++p) {
-        const int q = tid + p * NT, dg = q % KCH, kp = q / KCH;
-        const int r0 = q < VBLK ? 2 * kp : 0;
-        vreg[p][0] = *reinterpret_cast<const u32x4*>(vb + (r0 < nv_next ? r0 : 0) * rs + dg * 8);
-        vreg[p][1] = *reinterpret_cast<const u32x4*>(vb + (r0 + 1 < nv_next ? r0 + 1 : 0) * rs + dg * 8);
-      }
+    const bf16 *kb = (const bf16*)a.kp, *vb = (const bf16*)a.vp;
+    int bytes = 0;
+    if (t < TP) {
+      kb += g * a.p_sh + (long)t * KT * DH;
+      vb += g * a.p_sh + (long)t * KT * DH;
+      bytes = min(KT, a.m - t * KT) * DH * 2;
+    } else if (t < n_tiles) {
+      const int u = t - TP, rb = b_lo + u / TS, tt = u % TS;
+      const long off = rb * a.s_sb + g * a.s_sh + (long)tt * KT * DH;
+      kb = (const bf16*)a.ks + off;
+      vb = (const bf16*)a.vs + off;
+      bytes = min(KT, a.n_s - tt * KT) * DH * 2;
     }
+    const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kb), (short)0, bytes, RSRC_W3);
+    const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vb), (short)0, bytes, RSRC_W3);
+#pragma unroll
+    for (int p = 0; p < K_PER; ++p) kreg[p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
+    vreg[0] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off, 0, 0);
+    vreg[1] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off + DH * 2, 0, 0);
   };
-  auto stash = [&](int buf) __attribute__((always_inline)) {
-    if (nv_next < KT) {  // partial tile: zero the rows past the valid keys
+  auto stash = [&](int slot) __attribute__((always_inline)) {
+    bf16* base = smem + slot * SLOT;
 #pragma unroll
-      for (int p = 0; p < K_PER; ++p) {
-        const int r = (tid + p * NT) / KCH;
-        if (r >= nv_next) kreg[p] = zero4;
-      }
-#pragma unroll
-      for (int p = 0; p < V_PER; ++p) {
-        const int kp = (tid + p * NT) / KCH;
-        if (2 * kp >= nv_next) vreg[p][0] = zero4;
-        if (2 * kp + 1 >= nv_next) vreg[p][1] = zero4;
-      }
-    }
-#pragma unroll
-    for (int p = 0; p < K_PER; ++p) {
-      const int q = tid + p * NT, r = q / KCH, kc = q % KCH;
-      *reinterpret_cast<u32x4*>(&Ks[buf][kofs<KCH>(r, kc)]) = kreg[p];
-    }
-#pragma unroll
-    for (int p = 0; p < V_PER; ++p) {
-      const int q = tid + p * NT, dg = q % KCH, kp = q / KCH;
-      if (q >= VBLK) continue;
+    for (int p = 0; p < K_PER; ++p) *reinterpret_cast<u32x4*>(base + ks_off[p]) = kreg[p];
+    if (v_ok) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        // dim dg*8 + e of keys 2kp (low half) and 2kp+1 (high half), adjacent in V^T
-        const uint32_t w = __builtin_amdgcn_perm(vreg[p][1][e >> 1], vreg[p][0][e >> 1],
-                                                 (e & 1) ? 0x07060302u : 0x05040100u);
-        *reinterpret_cast<uint32_t*>(&Vt[buf][vofs(dg * 8 + e, 2 * kp)]) = w;
+        const uint32_t w = __builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], (e & 1) ? 0x07060302u : 0x05040100u);
+        *reinterpret_cast<uint32_t*>(base + vs_off + e * VROW) = w;
       }
     }
   };
 
-  f32x16 o[QB][NB];
-  float m_run[QB], l_run[QB];
+  f32x16 o[NB];
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb) o[qb][nb] = zero16();
-    m_run[qb] = -INFINITY;
-    l_run[qb] = 0.f;
-  }
-  const float sl2 = a.scale * 1.4426950408889634f;  // scale * log2(e)
+  for (int nb = 0; nb < NB; ++nb) o[nb] = zero16();
+  // finite start: a tile with every key masked leaves exp2 arguments at -inf
+  float m_run = -1e30f, l_run = 0.f;
+  const float sl2 = a.scale * 1.4426950408889634f;
+  const int k_rd = c * KROW + half * 8;                // lane's K fragment base
+  const int v_rd = KTILE + c * VROW + half * 8;        // lane's V^T fragment base
 
-  // Pipeline: registers hold tile t+1 while tile t computes; they are written
-  // to the other LDS buffer between tile t's S = K.Q^T and its softmax (that
-  // buffer was last read in tile t-1, before the previous barrier) and tile
-  // t+2 is fetched right after, so its loads have a whole tile to arrive.
-  fetch(0);
-  stash(0);
-  if (n_tiles > 1) fetch(1);
-  __syncthreads();
-
-  for (int t = 0; t < n_tiles; ++t) {
-    const int buf = t & 1;
-    int owner, nv;
-    {
-      const bf16 *kb, *vb;
-      long rs;
-      tile_src(t, kb, vb, rs, nv, owner);
-    }
-    const bool mine = active && (owner < 0 || owner == b);
-    // ---- S^T = K . Q^T over this tile's 64 keys; each K fragment feeds QB MFMAs
-    // (the first k step starts from a zero accumulator operand)
-    f32x16 sc[QB][KT / 32];
-    if (mine) {
+  auto pv = [&](int t, const bf16x8 (&p)[NS]) __attribute__((always_inline)) {
+    const bf16* vt = smem + (t % NBUF) * SLOT + v_rd;
 #pragma unroll
-      for (int kk = 0; kk < DH / 16; ++kk)
+    for (int s = 0; s < NS; ++s)
 #pragma unroll
-        for (int kb = 0; kb < KT / 32; ++kb) {
-          const int r = kb * 32 + c;
-          const bf16x8 kf =
-              *reinterpret_cast<const bf16x8*>(&Ks[buf][kofs<KCH>(r, kk * 2 + half)]);
-#pragma unroll
-          for (int qb = 0; qb < QB; ++qb)
-            sc[qb][kb] = mfma_32x32x16(kf, qf[qb][kk], kk == 0 ? zero16() : sc[qb][kb]);
-        }
-    }
-    if (t + 1 < n_tiles) {
-      stash(buf ^ 1);
-      if (t + 2 < n_tiles) fetch(t + 2);
-    }
-    if (mine) {
-      if (nv < KT) {
-#pragma unroll
-        for (int qb = 0; qb < QB; ++qb)
-#pragma unroll
-          for (int kb = 0; kb < KT / 32; ++kb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) {
-              const int key = kb * 32 + 8 * (e >> 2) + 4 * half + (e & 3);
-              if (key >= nv) sc[qb][kb][e] = -INFINITY;
-            }
+      for (int nb = 0; nb < NB; ++nb) {
+        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + s * 16);
+        o[nb] = mfma_32x32x16(vf, p[s], o[nb]);
       }
-      // ---- online softmax (log2 domain), one query row per lane per block
-      bf16x8 pf[QB][KT / 16];
-      const bf16x2 ones = {(bf16)1.f, (bf16)1.f};
+  };
+  auto qk = [&](int t, f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    const bf16* kt = smem + (t % NBUF) * SLOT + k_rd;
 #pragma unroll
-      for (int qb = 0; qb < QB; ++qb) {
-        float mx = -INFINITY;
+    for (int kk = 0; kk < NKK; ++kk)
 #pragma unroll
-        for (int kb = 0; kb < KT / 32; ++kb)
+      for (int kb = 0; kb < 2; ++kb) {
+        const bf16x8 kf = *reinterpret_cast<const bf16x8*>(kt + kb * 32 * KROW + kk * 16);
+        sc[kb] = mfma_32x32x16(kf, qf[kk], kk == 0 ? zero16() : sc[kb]);
+      }
+  };
+  // scores of a partial tile past its valid keys -> -inf; lane (half, c) holds
+  // key 32kb + 8(e/4) + 4half + e%4 of query row c in element e of block kb
+  // (branch-free bit select: compares would each hold a scalar mask)
+  auto mask = [&](f32x16 (&sc)[2], int nv) __attribute__((always_inline)) {
+    const int t = nv - 1 - 4 * half;
 #pragma unroll
-          for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[qb][kb][e]);
-        mx = half_max(mx) * sl2;
-        // The running max only moves when a row's tile max exceeds it by more
-        // than 8 (log2 units): probabilities then stay <= 2^8, exact in fp32
-        // and representable in bf16, and the O / l rescale is skipped on most
-        // tiles.
-        if (__builtin_amdgcn_ballot_w64(mx > m_run[qb] + 8.f)) {
-          const float m_new = fmaxf(m_run[qb], mx);
-          const float alpha = __builtin_amdgcn_exp2f(m_run[qb] - m_new);
-          l_run[qb] *= alpha;
-          m_run[qb] = m_new;
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int m = (t - (kb * 32 + 8 * (e >> 2) + (e & 3))) >> 31;   // -1: key >= nv
+        sc[kb][e] = __int_as_float((__float_as_int(sc[kb][e]) & ~m) | (int(0xff800000u) & m));
+      }
+  };
+  // the running max moves only when some row's tile max exceeds it by more
+  // than 8 (log2 units), so probabilities stay <= 2^8; returns the factor that
+  // moves O and the row sum to the new max (1 when it does not move)
+  auto new_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[kb][e]);
+    mx = half_max(mx) * sl2;
+    const bool move = __builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0;
+    const float m_new = move ? fmaxf(m_run, mx) : m_run;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    return alpha;
+  };
+  // P^T operand of k step s: slot (half, e) is key 16s + 8(e/4) + 4half +
+  // e%4, i.e. score element 8(s%2) + e of block s/2; lt accumulates the fp32
+  // probabilities (four partial sums)
+  auto probs = [&](const f32x16 (&sc)[2], int s, float (&lt)[4]) __attribute__((always_inline)) {
+    uint32_t pw[4];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      const int e0 = 8 * (s & 1) + 2 * w;
+      const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][e0], sl2, -m_run));
+      const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][e0 + 1], sl2, -m_run));
+      lt[w] += p0 + p1;
+      pw[w] = pack_bf16x2(p0, p1);
+    }
+    const u32x4 pv4 = {pw[0], pw[1], pw[2], pw[3]};
+    return __builtin_bit_cast(bf16x8, pv4);
+  };
+
+  // One step.  p holds P(u-1) on entry and P(u) on exit; sc holds S(u) on
+  // entry and S(u+1) on exit.  P(u)'s k step s replaces P(u-1)'s once the
+  // P.V MFMAs that read it have issued.  Tiles the wave does not own
+  // (another request's suffix) are fully masked, so their probabilities are
+  // zero and the P.V product adds nothing; every MFMA and vector instruction
+  // runs unconditionally, which keeps each block one straight-line region for
+  // the scheduler.
+  auto step = [&](int u, auto has_pv, auto has_qk, bf16x8 (&p)[NS], f32x16 (&sc)[2])
+      __attribute__((always_inline)) {
+    constexpr bool PV = decltype(has_pv)::value, QK = decltype(has_qk)::value;
+    float lt[4] = {0.f, 0.f, 0.f, 0.f};
+    const int nv = owns(u) ? valid_of(u) : 0;
+    if (nv < KT) mask(sc, nv);
+    // ---- block A: P(u-1).V(u-1) alongside the softmax of S(u), in NS
+    // fenced sub-blocks (k step s: its 4 MFMAs, then P(u)'s k step s in the
+    // registers they read), with the V fragments of step s+1 read one
+    // sub-block ahead
+    const bf16* vt = smem + ((u + NBUF - 1) % NBUF) * SLOT + v_rd;
+    bf16x8 vf[2][NB];
+    if constexpr (PV) {
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) vf[0][nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW);
+    }
+    float alpha = 1.f;
+#pragma unroll
+    for (int s = 0; s < NS; ++s) {
+      if constexpr (PV) {
+        if (s + 1 < NS) {
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-            for (int e = 0; e < 16; ++e) o[qb][nb][e] *= alpha;
+            vf[(s + 1) & 1][nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + (s + 1) * 16);
         }
-        // P^T operand of k step s: slot (half, e) is key 16s + 8*(e/4) +
-        // 4*half + e%4, i.e. score register 8*(s%2) + e of block s/2.  The row
-        // sum accumulates the same bf16-rounded probabilities that the P.V
-        // product uses (v_dot2 against (1, 1)); each dot2 takes its packed pair
-        // as its own value (taken back out of the 4-dword vector, the compiler
-        // feeds every dot2 the first element's register).
 #pragma unroll
-        for (int s = 0; s < KT / 16; ++s) {
-          uint32_t pw[4];
-#pragma unroll
-          for (int w = 0; w < 4; ++w) {
-            const int e0 = 8 * (s & 1) + 2 * w;
-            const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[qb][s >> 1][e0], sl2, -m_run[qb]));
-            const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[qb][s >> 1][e0 + 1], sl2, -m_run[qb]));
-            const bf16x2 pp = {(bf16)p0, (bf16)p1};
-            l_run[qb] = __builtin_amdgcn_fdot2_f32_bf16(pp, ones, l_run[qb], false);
-            pw[w] = __builtin_bit_cast(uint32_t, pp);
-          }
-          const u32x4 pv = {pw[0], pw[1], pw[2], pw[3]};
-          pf[qb][s] = __builtin_bit_cast(bf16x8, pv);
-        }
+        for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(vf[s & 1][nb], p[s], o[nb]);
       }
-
-      // ---- O^T += V^T . P^T, 16 keys per MFMA; each V^T fragment feeds QB MFMAs
+      if (s == 0) alpha = new_max(sc);
+      p[s] = probs(sc, s, lt);
+      // pin P(u)'s step s here: otherwise the compiler defers the softmax
+      // past block B and keeps a second copy of S(u) alive
+      asm volatile("" : "+v"(p[s]));
+      __builtin_amdgcn_sched_barrier(0);
+    }
+    if (alpha != 1.f) {
+      // rare: the running max moved; O already holds P(u-1).V(u-1)
 #pragma unroll
-      for (int s = 0; s < KT / 16; ++s) {
+      for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-        for (int nb = 0; nb < NB; ++nb) {
-          const int r = nb * 32 + c;
-          const bf16x8 vf =
-              *reinterpret_cast<const bf16x8*>(&Vt[buf][r * KT + (((2 * s + half) ^ vswz(r)) << 3)]);
+        for (int e = 0; e < 16; ++e) o[nb][e] *= alpha;
+    }
+    l_run = fmaf(l_run, alpha, (lt[0] + lt[1]) + (lt[2] + lt[3]));
+    // ---- block B: S(u+1) alongside the fill of tile u+2 (fetched last
+    // step) and the fetch of tile u+3
+    if constexpr (QK) qk(u + 1, sc);
+    stash((u + 2) % NBUF);
+    fetch(u + 3);
+    if constexpr (QK) {
+      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
 #pragma unroll
-          for (int qb = 0; qb < QB; ++qb) o[qb][nb] = mfma_32x32x16(vf, pf[qb][s], o[qb][nb]);
-        }
+      for (int i = 0; i < NKK * 2; ++i) {
+        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+        if (i + 4 < NKK * 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
       }
     }
+    // keep each step's work on its own side of the barrier
+    __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
-  }
+    __builtin_amdgcn_sched_barrier(0);
+  };
+  using T_ = std::true_type;
+  using F_ = std::false_type;
 
+  // prologue: tiles 0 and 1 in LDS, tile 2 in flight, S(0) computed
+  fetch(0);
+  stash(0);
+  fetch(1);
+  stash(1);
+  fetch(2);
+  __syncthreads();
+  bf16x8 p[NS];
+  f32x16 sc[2];
+  qk(0, sc);
+  // (the last step's S(n_tiles) reads a zero-filled slot and is discarded)
+  step(0, F_{}, T_{}, p, sc);
+  for (int u = 1; u < n_tiles; ++u) step(u, T_{}, T_{}, p, sc);
+  pv(n_tiles - 1, p);
+
+  if (!row_ok) return;
+  const float inv = 1.f / half_sum(l_run);
+  if constexpr (OUT_F32) {
+    float* op = (float*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
 #pragma unroll
-  for (int qb = 0; qb < QB; ++qb) {
-    if (!row_ok[qb]) continue;
-    const int qrow = i0 + 32 * qb + c;
-    const float l_tot = half_sum(l_run[qb]);
-    const float inv = 1.f / l_tot;
-    // lane holds O[row][dims nb*32 + 8j + 4*half + i], i = 0..3
-    if constexpr (OUT_F32) {
-      float* op = (float*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
+      for (int j = 0; j < 4; ++j) {
+        f32x4 v = {o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv, o[nb][4 * j + 2] * inv, o[nb][4 * j + 3] * inv};
+        *reinterpret_cast<f32x4*>(op + nb * 32 + 8 * j + 4 * half) = v;
+      }
+  } else {
+    bf16* op = (bf16*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
 #pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          f32x4 v = {o[qb][nb][4 * j] * inv, o[qb][nb][4 * j + 1] * inv, o[qb][nb][4 * j + 2] * inv,
-                     o[qb][nb][4 * j + 3] * inv};
-          *reinterpret_cast<f32x4*>(op + nb * 32 + 8 * j + 4 * half) = v;
-        }
-    } else {
-      bf16* op = (bf16*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
+    for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-          u32x2 v = {pack_bf16x2(o[qb][nb][4 * j] * inv, o[qb][nb][4 * j + 1] * inv),
-                     pack_bf16x2(o[qb][nb][4 * j + 2] * inv, o[qb][nb][4 * j + 3] * inv)};
-          *reinterpret_cast<u32x2*>(op + nb * 32 + 8 * j + 4 * half) = v;
-        }
-    }
+      for (int j = 0; j < 4; ++j) {
+        u32x2 v = {pack_bf16x2(o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv),
+                   pack_bf16x2(o[nb][4 * j + 2] * inv, o[nb][4 * j + 3] * inv)};
+        *reinterpret_cast<u32x2*>(op + nb * 32 + 8 * j + 4 * half) = v;
+      }
   }
 }
 
-template <int DH, int NW, int QB, bool F32>
-hipError_t launch_cfg(const AttnArgs& a, hipStream_t s) {
-  const int CQ = cdiv(a.n_s, 32 * QB);
-  const int G = a.Hq / a.Hkv;
-  const int wpg = cdiv(a.B * G * CQ, NW);
-  const int grid = a.Hkv * wpg;
-  hipLaunchKernelGGL((attn_kernel<DH, NW, QB, F32>), dim3(grid), dim3(NW * kWave), 0, s, a, CQ, wpg);
-  return hipGetLastError();
-}
-
-// 8 waves x 32 query rows per workgroup
 template <int DH, bool F32>
-hipError_t launch_dh(const AttnArgs& a, hipStream_t s) {
-  return launch_cfg<DH, 8, 1, F32>(a, s);
+hipError_t launch_il(const AttnArgs& a, hipStream_t s) {
+  if (a.s_sr != DH) return hipErrorInvalidValue;   // key rows must be dh apart
+  const int CQ = cdiv(a.n_s, 32);
+  const int G = a.Hq / a.Hkv;
+  const int wpg = cdiv(a.B * G * CQ, 8);
+  const int grid = a.Hkv * wpg;
+  if (grid == 0) return hipSuccess;
+  hipLaunchKernelGGL((attn_il_kernel<DH, F32>), dim3(grid), dim3(512), 0, s, a, CQ, wpg);
+  return hipGetLastError();
 }
 
 }  // namespace
 
 hipError_t attention(const AttnArgs& a, hipStream_t s) {
-  if (a.dh == 128) return a.out_f32 ? launch_dh<128, true>(a, s) : launch_dh<128, false>(a, s);
-  return a.out_f32 ? launch_dh<64, true>(a, s) : launch_dh<64, false>(a, s);
+  if (a.dh == 128) return a.out_f32 ? launch_il<128, true>(a, s) : launch_il<128, false>(a, s);
+  return a.out_f32 ? launch_il<64, true>(a, s) : launch_il<64, false>(a, s);
 }
 
 }  // namespace bc
