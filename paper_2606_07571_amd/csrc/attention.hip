@@ -180,7 +180,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   f32x16 o[NB];
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) o[nb] = zero16();
-  // finite start: a tile with every key masked leaves exp2 arguments at -inf
+  // running row max m (log2 units) and row sum l
   float m_run = -1e30f, l_run = 0.f;
   const float sl2 = a.scale * 1.4426950408889634f;
   const int k_rd = c * KROW + half * 8;                // lane's K fragment base
@@ -219,22 +219,6 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
         sc[kb][e] = __int_as_float((__float_as_int(sc[kb][e]) & ~m) | (int(0xff800000u) & m));
       }
   };
-  // the running max moves only when some row's tile max exceeds it by more
-  // than 8 (log2 units), so probabilities stay <= 2^8; returns the factor that
-  // moves O and the row sum to the new max (1 when it does not move)
-  auto new_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
-    float mx = -INFINITY;
-#pragma unroll
-    for (int kb = 0; kb < 2; ++kb)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[kb][e]);
-    mx = half_max(mx) * sl2;
-    const bool move = __builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0;
-    const float m_new = move ? fmaxf(m_run, mx) : m_run;
-    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
-    m_run = m_new;
-    return alpha;
-  };
   // P^T operand of k step s: slot (half, e) is key 16s + 8(e/4) + 4half +
   // e%4, i.e. score element 8(s%2) + e of block s/2; lt accumulates the fp32
   // probabilities (four partial sums)
@@ -251,69 +235,111 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     const u32x4 pv4 = {pw[0], pw[1], pw[2], pw[3]};
     return __builtin_bit_cast(bf16x8, pv4);
   };
+  // The running max moves only when some row's tile max exceeds it by more
+  // than 8 (log2 units), so probabilities stay <= 2^8; returns the factor
+  // that moves O and the row sum to the new max (1 when it does not move).
+  // The first tile of a row always moves it (m starts at -inf, kept finite
+  // so that fully masked tiles give exp2(-inf) = 0).
+  auto new_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
+    float mx = -INFINITY;
+#pragma unroll
+    for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+      for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[kb][e]);
+    mx = half_max(mx) * sl2;
+    const bool move = __builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0;
+    const float m_new = move ? fmaxf(m_run, mx) : m_run;
+    const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+    m_run = m_new;
+    return alpha;
+  };
 
-  // One step.  p holds P(u-1) on entry and P(u) on exit; sc holds S(u) on
-  // entry and S(u+1) on exit.  P(u)'s k step s replaces P(u-1)'s once the
-  // P.V MFMAs that read it have issued.  Tiles the wave does not own
-  // (another request's suffix) are fully masked, so their probabilities are
-  // zero and the P.V product adds nothing; every MFMA and vector instruction
-  // runs unconditionally, which keeps each block one straight-line region for
-  // the scheduler.
-  auto step = [&](int u, auto has_pv, auto has_qk, bf16x8 (&p)[NS], f32x16 (&sc)[2])
+  // One step, as a chain of fenced sub-blocks of (up to) 4 MFMAs each: NS
+  // P.V sub-blocks (k step s of P(u-1).V(u-1)) and NKK/2 QK sub-blocks (k
+  // steps 2j, 2j+1 of S(u+1)).  Each sub-block first issues the LDS fragment
+  // reads of the next one (the last reads the next step's first), then its
+  // MFMAs interleaved with its share of the vector work, so fragment reads
+  // have a whole sub-block to arrive and a wave never waits on LDS with
+  // independent work queued behind the wait.
+  //   P.V sub-block s:   softmax of S(u): the row max and running max (s = 0)
+  //                      and P(u)'s k step s, written into the registers the
+  //                      sub-block's MFMAs have just read
+  //   QK sub-blocks:     LDS fill of tile u+2, fetch of tile u+3
+  // p holds P(u-1) on entry and P(u) on exit; sc holds S(u) on entry and
+  // S(u+1) on exit; fr[0] holds the first sub-block's fragments on entry and
+  // the next step's on exit.  Tiles the wave does not own (another request's
+  // suffix) are fully masked, so their probabilities are zero and the P.V
+  // product adds nothing; every MFMA and vector instruction runs
+  // unconditionally.
+  constexpr int NQS = NKK / 2;                  // QK sub-blocks
+  constexpr int NSUB = NS + NQS;
+  static_assert(NSUB % 2 == 0, "fragment double buffer parity");
+  auto load_sub = [&](int j, int u, bf16x8 (&f)[4]) __attribute__((always_inline)) {
+    if (j < NS) {
+      const bf16* vt = smem + ((u + NBUF - 1) % NBUF) * SLOT + v_rd;
+#pragma unroll
+      for (int nb = 0; nb < NB; ++nb) f[nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + j * 16);
+    } else {
+      const bf16* kt = smem + ((u + 1) % NBUF) * SLOT + k_rd;
+      const int kk0 = 2 * (j - NS);
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        f[i] = *reinterpret_cast<const bf16x8*>(kt + (i & 1) * 32 * KROW + (kk0 + (i >> 1)) * 16);
+    }
+  };
+  auto step = [&](int u, auto has_pv, bf16x8 (&p)[NS], f32x16 (&sc)[2], bf16x8 (&fr)[2][4])
       __attribute__((always_inline)) {
-    constexpr bool PV = decltype(has_pv)::value, QK = decltype(has_qk)::value;
+    constexpr bool PV = decltype(has_pv)::value;
     float lt[4] = {0.f, 0.f, 0.f, 0.f};
     const int nv = owns(u) ? valid_of(u) : 0;
     if (nv < KT) mask(sc, nv);
-    // ---- block A: P(u-1).V(u-1) alongside the softmax of S(u), in NS
-    // fenced sub-blocks (k step s: its 4 MFMAs, then P(u)'s k step s in the
-    // registers they read), with the V fragments of step s+1 read one
-    // sub-block ahead
-    const bf16* vt = smem + ((u + NBUF - 1) % NBUF) * SLOT + v_rd;
-    bf16x8 vf[2][NB];
-    if constexpr (PV) {
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb) vf[0][nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW);
-    }
+    if constexpr (!PV) load_sub(NS, u, fr[NS & 1]);
     float alpha = 1.f;
 #pragma unroll
-    for (int s = 0; s < NS; ++s) {
-      if constexpr (PV) {
-        if (s + 1 < NS) {
+    for (int j = 0; j < NSUB; ++j) {
+      if (PV || j >= NS) {
+        if (j + 1 < NSUB) load_sub(j + 1, u, fr[(j + 1) & 1]);
+        else load_sub(0, u + 1, fr[0]);
+      }
+      if (j < NS) {
+        if constexpr (PV) {
+#pragma unroll
+          for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(fr[j & 1][nb], p[j], o[nb]);
+        }
+        if (j == 0) alpha = new_max(sc);
+        p[j] = probs(sc, j, lt);
+        // pin P(u)'s step j here: otherwise the compiler defers the softmax
+        // past the QK MFMAs and keeps a second copy of S(u) alive
+        asm volatile("" : "+v"(p[j]));
+      } else {
+        const int kk0 = 2 * (j - NS);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          const int kk = kk0 + (i >> 1), kb = i & 1;
+          sc[kb] = mfma_32x32x16(fr[j & 1][i], qf[kk], kk == 0 ? zero16() : sc[kb]);
+        }
+        if (j == NS) stash((u + 2) % NBUF);
+        if (j == NS + 1 || (NQS == 1 && j == NS)) fetch(u + 3);
+      }
+      // reads first, then MFMAs each followed by a share of the VALU work
+      if (PV || j >= NS) {
+        __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
+#pragma unroll
+        for (int i = 0; i < 4; ++i) {
+          __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
+          __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
+        }
+      }
+      __builtin_amdgcn_sched_barrier(0);
+      if (j == NS - 1) {
+        if (alpha != 1.f) {
+          // rare: the running max moved; O already holds P(u-1).V(u-1)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
-            vf[(s + 1) & 1][nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + (s + 1) * 16);
+#pragma unroll
+            for (int e = 0; e < 16; ++e) o[nb][e] *= alpha;
         }
-#pragma unroll
-        for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(vf[s & 1][nb], p[s], o[nb]);
-      }
-      if (s == 0) alpha = new_max(sc);
-      p[s] = probs(sc, s, lt);
-      // pin P(u)'s step s here: otherwise the compiler defers the softmax
-      // past block B and keeps a second copy of S(u) alive
-      asm volatile("" : "+v"(p[s]));
-      __builtin_amdgcn_sched_barrier(0);
-    }
-    if (alpha != 1.f) {
-      // rare: the running max moved; O already holds P(u-1).V(u-1)
-#pragma unroll
-      for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-        for (int e = 0; e < 16; ++e) o[nb][e] *= alpha;
-    }
-    l_run = fmaf(l_run, alpha, (lt[0] + lt[1]) + (lt[2] + lt[3]));
-    // ---- block B: S(u+1) alongside the fill of tile u+2 (fetched last
-    // step) and the fetch of tile u+3
-    if constexpr (QK) qk(u + 1, sc);
-    stash((u + 2) % NBUF);
-    fetch(u + 3);
-    if constexpr (QK) {
-      __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
-#pragma unroll
-      for (int i = 0; i < NKK * 2; ++i) {
-        __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
-        if (i + 4 < NKK * 2) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
-        __builtin_amdgcn_sched_group_barrier(0x002, 2, 0);
+        l_run = fmaf(l_run, alpha, (lt[0] + lt[1]) + (lt[2] + lt[3]));
       }
     }
     // keep each step's work on its own side of the barrier
@@ -333,10 +359,11 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   __syncthreads();
   bf16x8 p[NS];
   f32x16 sc[2];
+  bf16x8 fr[2][4];
   qk(0, sc);
   // (the last step's S(n_tiles) reads a zero-filled slot and is discarded)
-  step(0, F_{}, T_{}, p, sc);
-  for (int u = 1; u < n_tiles; ++u) step(u, T_{}, T_{}, p, sc);
+  step(0, F_{}, p, sc, fr);
+  for (int u = 1; u < n_tiles; ++u) step(u, T_{}, p, sc, fr);
   pv(n_tiles - 1, p);
 
   if (!row_ok) return;
