@@ -45,6 +45,26 @@ def step_flops(cfg, B, m, n_s, d):
     return d * shallow + (L - d) * deep
 
 
+TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_swiglu_c3_step_d8_traffic.md")
+GEMM_SOURCE = os.path.join(ROOT, "paper_2606_07571_amd", "csrc", "gemm.hip")
+
+
+def measured_traffic(d):
+    """HBM bytes per gate_up launch from the committed rocprofv3 counter
+    summary (FETCH_SIZE + WRITE_SIZE, scaled by the copy calibration), or None
+    when there is none for this depth or the GEMM source changed since."""
+    import hashlib
+    try:
+        txt = open(TRAFFIC_PROFILE).read()
+        fields = dict(line.split(":", 1) for line in txt.splitlines() if line.startswith(("bytes_per_launch:", "gemm_source_sha256:", "depth:")))
+        sha = hashlib.sha256(open(GEMM_SOURCE, "rb").read()).hexdigest()
+        if fields.get("gemm_source_sha256", "").strip() != sha or int(fields.get("depth", "-1")) != d:
+            return None
+        return int(float(fields["bytes_per_launch"]))
+    except (OSError, KeyError, ValueError):
+        return None
+
+
 def gate_up_flops(cfg, rows):
     return 2.0 * rows * 2 * cfg["ffn"] * cfg["hidden"]
 
@@ -57,6 +77,9 @@ def main():
     ap.add_argument("--depth", type=int, default=8)
     ap.add_argument("--depth-steps", type=int, default=3, help="timed steps per extra depth")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--profile-step", action="store_true",
+                    help="run one warm step at --depth plus a 512 MiB copy (counter calibration) and exit; "
+                         "the command profiled under rocprofv3")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -87,6 +110,19 @@ def main():
     model.populate(key, xp, L)
     torch.cuda.synchronize()
     out = torch.empty((B, n_s, cfg["hidden"]), dtype=torch.float32, device=dev)
+
+    if args.profile_step:
+        model.step(key, xs, d, out=out)
+        model.step(key, xs, d, out=out)
+        # plain copy of known size: 512 MiB read + 512 MiB written, the
+        # reference that scales the HBM byte counters
+        src = torch.empty(256 * 2 ** 20, dtype=torch.float16, device=dev).fill_(1.0)
+        dst = torch.empty_like(src)
+        dst.copy_(src)
+        torch.cuda.synchronize()
+        log(f"bench: profile step done (d={d}; calibration copy {src.numel() * 2} bytes)")
+        model.close()
+        return
 
     # populate timing (prefix-only forward of all 32 layers, m = 1536)
     model.invalidate(key)
@@ -121,7 +157,7 @@ def main():
     gu_tflops = gu_flops / (gu_ms / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": "gate_up_swiglu GEMM (bf16 MFMA)",
                 "achieved": round(gu_tflops, 1), "peak": PEAK_BF16_TFLOPS, "unit": "TFLOP/s",
-                "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4), "traffic": None,
+                "frac": round(gu_tflops / PEAK_BF16_TFLOPS, 4), "traffic": measured_traffic(d),
                 "launches": gu_n, "avg_launch_ms": round(gu_ms / gu_n, 4)}
 
     # per-kernel breakdown of one extra profiled step (all classes)
