@@ -19,6 +19,10 @@ GPU receives, widened exactly):
   suffix rows (Eq. 4); layers l >= d recompute the prefix from the current
   request and run full bidirectional attention (refresh case of Eq. 5).
   d is the paper's b (its layers are 1-based, l <= b; here 0-based, l < d).
+* step_reuse_one / denoise_steps: the steps between refreshes (second case
+  of Eq. 5, refresh every delta steps, (t - 1) mod delta == 0): every layer
+  is suffix-only, the deep layers attending over the prefix K/V that the
+  request's last refresh step computed.
 * full_forward: the un-cached forward of (p, z_t) ("no caching"), which is
   what d = 0 must equal.
 
@@ -212,6 +216,58 @@ def step_one(cache, s0, d, layers, cfg, record=None):
             record.setdefault("deep_k", {})[l] = k[:, :m]
             record.setdefault("deep_v", {})[l] = v[:, :m]
     return x[m:]
+
+
+def is_refresh_step(t, delta):
+    """Eq. 5: step t (1-based) recomputes the deep layers' prefix KVs when
+    (t - 1) mod delta == 0; otherwise they are reused from the previous step."""
+    assert t >= 1 and delta >= 1
+    return (t - 1) % delta == 0
+
+
+def step_reuse_one(cache, deep, s0, d, layers, cfg):
+    """A non-refresh step of ONE request (Eq. 4 for l < d, the second case of
+    Eq. 5 for l >= d): every layer is suffix-only.  Shallow layers attend over
+    the shared cache["k"/"v"][l]; deep layers over the request's own prefix
+    K/V of its last refresh step, deep["deep_k"][l] / deep["deep_v"][l]
+    ([Hkv, m, dh], as recorded by step_one).  Returns the suffix rows' final
+    residual [n_s, h]."""
+    L = cfg["n_layers"]
+    m = cache["m"]
+    s = np.asarray(s0, dtype=np.float64)
+    suf_pos = m + np.arange(s.shape[0])
+    for l in range(L):
+        if l < d:
+            kp, vp = cache["k"][l], cache["v"][l]
+        else:
+            kp, vp = deep["deep_k"][l], deep["deep_v"][l]
+        s, _, _ = layer_suffix(s, layers[l], cfg, kp, vp, suf_pos)
+    return s
+
+
+def denoise_steps(cache, x_suffix_steps, d, delta, layers, cfg):
+    """Steps t = 1..T of a batch under Eq. 4/5 with refresh interval delta.
+
+    x_suffix_steps: [T, B, n_s, h], the suffix input of every step.  Refresh
+    steps run step_one (deep layers recompute the prefix from the cached
+    prefix-only residual) and record each request's deep prefix K/V; the
+    other steps run step_reuse_one with the latest record.  Returns
+    [T, B, n_s, h]."""
+    T, B = x_suffix_steps.shape[0], x_suffix_steps.shape[1]
+    deep = [None] * B
+    out = []
+    for t in range(1, T + 1):
+        xs = x_suffix_steps[t - 1]
+        row = []
+        for b in range(B):
+            if is_refresh_step(t, delta):
+                rec = {}
+                row.append(step_one(cache, xs[b], d, layers, cfg, record=rec))
+                deep[b] = rec
+            else:
+                row.append(step_reuse_one(cache, deep[b], xs[b], d, layers, cfg))
+        out.append(np.stack(row))
+    return np.stack(out)
 
 
 def step(cache, x_suffix, d, layers, cfg, requests=None):

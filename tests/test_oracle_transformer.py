@@ -249,3 +249,110 @@ def test_partial_populate_layout(setup):
     none = T.populate(xp, layers, cfg, 0)
     assert none["k"].shape[0] == 0 and none["h"].shape[0] == 1
     np.testing.assert_array_equal(none["h"][0], xp)
+
+
+# ---------------------------------------------------------------- Eq. 5 reuse
+
+def test_refresh_schedule_closed_forms():
+    """Eq. 5: step 1 refreshes; with delta = 16 the refresh steps of a 128-step
+    generation are 1, 17, ..., 113 (eight of them, ceil(T / delta) in general);
+    delta = 1 refreshes at every step."""
+    assert T.is_refresh_step(1, 16)
+    assert [t for t in range(1, 129) if T.is_refresh_step(t, 16)] == [1 + 16 * i for i in range(8)]
+    for delta in (1, 2, 3, 7, 16, 64):
+        for n in (1, 5, 16, 17, 128):
+            assert sum(T.is_refresh_step(t, delta) for t in range(1, n + 1)) == -(-n // delta)
+    assert all(T.is_refresh_step(t, 1) for t in range(1, 50))
+    # a refresh is followed by exactly delta - 1 reuse steps
+    assert not any(T.is_refresh_step(t, 4) for t in (2, 3, 4)) and T.is_refresh_step(5, 4)
+
+
+def test_reuse_right_after_refresh_is_exact(setup):
+    """The suffix rows of a full layer attend over [prefix K/V ; suffix K/V], so
+    feeding the refresh step's own prefix K/V back with the same suffix input
+    reproduces the refresh output for every depth."""
+    cfg, layers, xp, xs, cache = setup
+    for d in range(cfg["n_layers"] + 1):
+        for b in range(xs.shape[0]):
+            rec = {}
+            ref = T.step_one(cache, xs[b], d, layers, cfg, record=rec)
+            got = T.step_reuse_one(cache, rec, xs[b], d, layers, cfg)
+            np.testing.assert_allclose(got, ref, atol=1e-12)
+
+
+def test_reuse_uses_own_deep_layers_only(setup):
+    """Shallow layers read the shared cache, deep layers only the request's own
+    record: poisoning the record below d changes nothing, poisoning it at any
+    deep layer poisons the output, and another request's record is not
+    interchangeable."""
+    cfg, layers, xp, xs, cache = setup
+    L = cfg["n_layers"]
+    d = 1
+    rec0, rec1 = {}, {}
+    T.step_one(cache, xs[0], d, layers, cfg, record=rec0)
+    T.step_one(cache, xs[1], d, layers, cfg, record=rec1)
+    ref = T.step_reuse_one(cache, rec0, xs[2], d, layers, cfg)
+    assert set(rec0["deep_k"]) == set(range(d, L))
+    for l in range(d, L):
+        bad = {"deep_k": dict(rec0["deep_k"]), "deep_v": dict(rec0["deep_v"])}
+        bad["deep_v"][l] = np.full_like(bad["deep_v"][l], np.nan)
+        assert np.isnan(T.step_reuse_one(cache, bad, xs[2], d, layers, cfg)).all()
+    other = T.step_reuse_one(cache, rec1, xs[2], d, layers, cfg)
+    assert np.abs(other - ref).max() > 1e-6
+    # the stale prefix K/V make a reuse step differ from a fresh recompute
+    assert np.abs(T.step_one(cache, xs[2], d, layers, cfg) - ref).max() > 1e-6
+    # at d = L there are no deep layers and the record is never read
+    np.testing.assert_array_equal(T.step_reuse_one(cache, {}, xs[2], L, layers, cfg),
+                                  T.step_one(cache, xs[2], L, layers, cfg))
+
+
+def test_first_layer_reuse_is_exact_for_any_suffix():
+    """Footnote of Sec. 4.2: first-layer prefix K/V depend on the prefix tokens
+    alone, so in a one-layer model with d = 0 reusing them across steps is
+    exact whatever the new suffix."""
+    cfg = _cfg(n_layers=1)
+    rng = np.random.default_rng(6)
+    layers = _weights(cfg, rng)
+    xp, xs = rng.normal(size=(6, 32)), rng.normal(size=(2, 4, 32))
+    cache = T.populate(xp, layers, cfg, 1)
+    rec = {}
+    T.step_one(cache, xs[0], 0, layers, cfg, record=rec)
+    np.testing.assert_allclose(T.step_reuse_one(cache, rec, xs[1], 0, layers, cfg),
+                               T.step_one(cache, xs[1], 0, layers, cfg), atol=1e-12)
+
+
+def test_denoise_steps_schedule(setup):
+    """delta = 1 is a refresh at every step (plain step per step); with delta = 3
+    the refresh steps 1 and 4 match a fresh step of their own input whatever
+    came before, and the reuse steps 2, 3, 5 depend on the inputs of their
+    last refresh step but not on those of earlier reuse steps."""
+    cfg, layers, xp, xs, cache = setup
+    rng = np.random.default_rng(7)
+    n_steps, d = 5, 1
+    xsteps = xs[None] + 0.3 * rng.normal(size=(n_steps,) + xs.shape)
+    every = T.denoise_steps(cache, xsteps, d, 1, layers, cfg)
+    for t in range(n_steps):
+        np.testing.assert_allclose(every[t], T.step(cache, xsteps[t], d, layers, cfg), atol=1e-12)
+    base = T.denoise_steps(cache, xsteps, d, 3, layers, cfg)
+    for t in (0, 3):
+        np.testing.assert_allclose(base[t], every[t], atol=1e-12)
+    for t in (1, 2, 4):
+        assert np.abs(base[t] - every[t]).max() > 1e-6
+    # changing the input of reuse step 2 changes step 2 only
+    x2 = xsteps.copy()
+    x2[1] += 1.0
+    alt = T.denoise_steps(cache, x2, d, 3, layers, cfg)
+    assert np.abs(alt[1] - base[1]).max() > 1e-6
+    for t in (0, 2, 3, 4):
+        np.testing.assert_array_equal(alt[t], base[t])
+    # changing the input of refresh step 1 changes every step up to step 4
+    x1 = xsteps.copy()
+    x1[0] += 1.0
+    alt = T.denoise_steps(cache, x1, d, 3, layers, cfg)
+    for t in (0, 1, 2):
+        assert np.abs(alt[t] - base[t]).max() > 1e-6
+    for t in (3, 4):
+        np.testing.assert_array_equal(alt[t], base[t])
+    # requests stay independent across the whole sequence
+    one = T.denoise_steps(cache, xsteps[:, 1:2], d, 3, layers, cfg)
+    np.testing.assert_allclose(one[:, 0], base[:, 1], atol=1e-13)
