@@ -15,8 +15,9 @@ Workload (one "step" = one bc_step_forward call, the whole hot path):
 Prints ONE JSON line: request-denoise-steps/s of that step (value), the
 roofline of its dominant kernel (the gate/up + SwiGLU GEMM) measured live with
 HIP events inside the timed region, the fp64 CPU oracle timed on a bounded
-sample (rank 0), plus the per-depth step times and the shared-prefix attention
-throughput of the attention-only workloads.
+sample (rank 0), plus the per-depth step times, the deep-layer reuse steps of
+Eq. 5 (refresh, reuse, and their mix at refresh interval 16), and the
+shared-prefix attention throughput of the attention-only workloads.
 """
 import argparse
 import json
@@ -185,6 +186,41 @@ def main():
         r["speedup_vs_d0"] = round(base / r["ms"], 3)
         r["ideal_speedup"] = round(f0 / step_flops(cfg, B, m, n_s, dd), 3)
 
+    # ------------------------------------------------ deep-layer reuse (Eq. 5)
+    # refresh steps write the deep layers' K/V into a per-batch store; the
+    # steps in between run every layer on the suffix rows only.  Amortized over
+    # a refresh interval of 16 (one refresh, 15 reuse steps).
+    def timed(fn, n):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(n):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / n
+
+    delta = 16
+    deep_reuse = {}
+    for dd in sorted(set([0, d])):
+        if dd >= L:
+            continue
+        store = model.new_deep_store(key, B, n_s, dd, device=dev)
+        t_ref = timed(lambda: model.step(key, xs, dd, out=out, deep="refresh", deep_store=store),
+                      args.depth_steps)
+        t_reu = timed(lambda: model.step(key, xs, dd, out=out, deep="reuse", deep_store=store),
+                      args.depth_steps)
+        amort = (t_ref + (delta - 1) * t_reu) / delta
+        deep_reuse[dd] = {"refresh_ms": round(t_ref, 3), "reuse_ms": round(t_reu, 3),
+                          "reuse_tflops": round(step_flops(cfg, B, m, n_s, L) / (t_reu / 1e3) / 1e12, 1),
+                          "delta": delta, "amortized_ms": round(amort, 3),
+                          "request_steps_per_s": round(B / (amort / 1e3), 2),
+                          "speedup_vs_d0": round(per_depth[0]["ms"] / amort, 3),
+                          "store_gib": round(store.numel() / 2 ** 30, 2)}
+        del store
+        torch.cuda.empty_cache()
+
     # C4 populate: 8 layers of the same shape over an 8192-token prefix
     xp4 = synth.gaussian((8192, cfg["hidden"]), 4100, device=dev)
     key4 = bc.prefix_key(range(8192))
@@ -251,6 +287,7 @@ def main():
         "roofline": roofline,
         "cpu_baseline": cpu,
         "per_depth": per_depth,
+        "deep_reuse": deep_reuse,
         "kernel_ms_one_step": breakdown,
         "attention": attention,
         "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},

@@ -187,13 +187,82 @@ bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int*
 bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
                           int d, float* out, void* workspace, size_t ws_bytes, void* stream);
 
+/* ------------------------------------------------- deep-layer reuse (Eq. 5)
+ *
+ * Within one request the deep layers (l >= d) need not recompute the prefix
+ * at every step (Sec. 5.2, Eq. 5): at a refresh step, (t - 1) mod delta == 0
+ * with t the 1-based step index and delta the refresh interval, they
+ * recompute it (exactly bc_step_forward); at every other step they reuse the
+ * prefix K/V that the request's last refresh step computed, so the whole step
+ * runs on the suffix rows only.  Those K/V live in a caller-owned "deep
+ * store", one per batch of requests that step together. */
+
+/* 1 if step t (1-based) of a request is a refresh step for refresh interval
+ * delta, i.e. (t - 1) mod delta == 0; 0 if it reuses; -1 if t < 1 or
+ * delta < 1.  Host only. */
+int bc_is_refresh_step(int t, int delta);
+
+enum {
+  BC_DEEP_REFRESH = 0, /* first case of Eq. 5: deep layers recompute the prefix */
+  BC_DEEP_REUSE = 1    /* second case: deep layers attend over the stored prefix K/V */
+};
+
+/* Device bytes of the deep store of a batch of B requests with n_s suffix rows
+ * each over a prefix of m tokens at reuse depth d.  Layout: for each deep
+ * layer l = d..L-1, K then V, each [B][Hkv][m + n_s][dh] bf16 (post-RoPE, the
+ * refresh step's K/V of every row of the request; reuse steps read rows
+ * 0..m-1).  Returns 0 for invalid arguments and for d = L (no deep layers). */
+size_t bc_deep_store_bytes(const bc_model* model, int m, int B, int n_s, int d);
+
+/* Byte offset inside a deep store of element (layer, part, req, head, pos,
+ * dim): d <= layer < L, part 0 = K / 1 = V, req < B, head < Hkv,
+ * pos < m + n_s, dim < dh.  Returns (size_t)-1 when out of range. */
+size_t bc_deep_store_offset(const bc_model* model, int m, int B, int n_s, int d, int layer,
+                            int part, int req, int head, int pos, int dim);
+
+/* Drops the tag of the deep store at `deep_store` (see bc_step_forward_deep),
+ * so that a reuse step on it is refused until a refresh step writes it again.
+ * Call it whenever memory at that address is newly allocated or put to other
+ * use: the tag is keyed by address, and allocators hand addresses out again.
+ * Returns BC_OK whether or not the address was tagged.  Host only. */
+bc_status bc_deep_store_reset(bc_model* model, const void* deep_store);
+
+/* One denoising step of B requests sharing the cached prefix `key`, with the
+ * deep layers in either case of Eq. 5.
+ *   mode BC_DEEP_REFRESH: the same computation and output as bc_step_forward;
+ *        if deep_store is not NULL, the deep layers' K/V of every row are
+ *        written into it (layout above) and the store is tagged with
+ *        (key, m, B, n_s, d).  deep_store may be NULL (nothing is stored).
+ *   mode BC_DEEP_REUSE: every layer runs on the suffix rows only (positions
+ *        m..m+n_s-1).  Layers l < d attend over [KV$_l ; own suffix K/V]
+ *        (Eq. 4), layers l >= d over [request b's prefix rows of the deep
+ *        store ; own suffix K/V].  The store is only read.  The store must
+ *        carry the tag of a refresh step with the same key, m, B, n_s and d
+ *        (else BC_E_STATE); request b of this call must be request b of that
+ *        refresh.  The library keeps the tag on the host, keyed by the store's
+ *        address: it cannot tell whether the memory was overwritten since
+ *        (bc_deep_store_reset drops the tag).
+ *   At d = L there are no deep layers: both modes equal bc_step_forward and
+ *   deep_store is ignored (may be NULL).
+ *   deep_store  device, >= bc_deep_store_bytes(model, m, B, n_s, d) bytes,
+ *               256-byte aligned, caller-owned
+ *   workspace   device, >= bc_step_workspace_bytes(model, m, B, n_s, d) bytes
+ *               (a reuse step needs no more than
+ *               bc_step_workspace_bytes(model, m, B, n_s, L))
+ * Other arguments and errors as bc_step_forward; a refresh of a batch is for
+ * all its requests at once (per-request schedules need separate batches). */
+bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suffix, int B,
+                               int n_s, int d, int mode, void* deep_store, size_t store_bytes,
+                               float* out, void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------------------ profiling */
 
 /* Kernel classes of the step and of populate, for bc_profile_* below. */
 enum {
   BC_K_RMSNORM = 0,     /* RMSNorm (both norms of a layer) */
   BC_K_QKV = 1,         /* fused Q/K/V projection + RoPE (+ cache write in populate) */
-  BC_K_ATTN_SHARED = 2, /* attention over [shared prefix ; own suffix] (layers l < d) */
+  BC_K_ATTN_SHARED = 2, /* attention over [cached prefix ; own suffix]: layers l < d,
+                           and every layer of a reuse step */
   BC_K_ATTN_FULL = 3,   /* full attention of each request (layers l >= d, populate) */
   BC_K_OPROJ = 4,       /* output projection + residual add */
   BC_K_GATE_UP = 5,     /* gate/up projection + SwiGLU */
@@ -229,6 +298,20 @@ bc_status bc_shared_prefix_attention(const void* q, const void* k_pre, const voi
                                      const void* k_suf, const void* v_suf, float* out, int B,
                                      int Hq, int Hkv, int m, int n_s, int dh, float scale,
                                      void* stream);
+
+/* Attention over [each request's own prefix ; own suffix] (Eq. 2, the deep
+ * layers of a reuse step, second case of Eq. 5), one launch:
+ *   out[b,j,i,:] = sum_t softmax_t(scale * q[b,j,i,:] . K_t) V_t
+ * over the keys t of [k_pre[b,g] ; k_suf[b,g]] with g = j / (Hq/Hkv); no mask.
+ *   q            bf16 [B, Hq, n_s, dh]
+ *   k_pre, v_pre bf16 [B, Hkv, m, dh]   request b's prefix K/V (m >= 0)
+ *   k_suf, v_suf bf16 [B, Hkv, n_s, dh]
+ *   out          fp32 [B, Hq, n_s, dh]
+ * Sizes, precision and errors as bc_shared_prefix_attention. */
+bc_status bc_request_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
+                                      const void* k_suf, const void* v_suf, float* out, int B,
+                                      int Hq, int Hkv, int m, int n_s, int dh, float scale,
+                                      void* stream);
 
 #ifdef __cplusplus
 }

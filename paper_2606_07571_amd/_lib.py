@@ -58,6 +58,14 @@ _SIGS = {
     "bc_step_forward": (C.c_int, [C.c_void_p, C.c_uint64, C.c_void_p, C.c_int, C.c_int, C.c_int,
                                   C.c_void_p, C.c_void_p, C.c_size_t, C.c_void_p]),
     "bc_shared_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
+    "bc_request_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
+    "bc_is_refresh_step": (C.c_int, [C.c_int, C.c_int]),
+    "bc_deep_store_reset": (C.c_int, [C.c_void_p, C.c_void_p]),
+    "bc_deep_store_bytes": (C.c_size_t, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int]),
+    "bc_deep_store_offset": (C.c_size_t, [C.c_void_p] + [C.c_int] * 10),
+    "bc_step_forward_deep": (C.c_int, [C.c_void_p, C.c_uint64, C.c_void_p, C.c_int, C.c_int, C.c_int,
+                                       C.c_int, C.c_void_p, C.c_size_t, C.c_void_p, C.c_void_p,
+                                       C.c_size_t, C.c_void_p]),
     "bc_profile_begin": (C.c_int, [C.c_void_p, C.c_uint]),
     "bc_profile_end": (C.c_int, [C.c_void_p, C.POINTER(C.c_double), C.POINTER(C.c_int)]),
 }
@@ -129,6 +137,35 @@ def shared_prefix_attention(q, k_pre, v_pre, k_suf, v_suf, scale=None, out=None)
     _check(lib().bc_shared_prefix_attention(*args, B, Hq, Hkv, m, n_s, dh, float(scale), _stream()))
     return out
 
+
+def request_prefix_attention(q, k_pre, v_pre, k_suf, v_suf, scale=None, out=None):
+    """One launch of the attention kernel with a per-request prefix.
+
+    q [B,Hq,n_s,dh], k_pre/v_pre [B,Hkv,m,dh], k_suf/v_suf [B,Hkv,n_s,dh]
+    (bf16, device); returns out fp32 [B,Hq,n_s,dh].
+    """
+    B, Hq, n_s, dh = q.shape
+    Hkv, m = k_pre.shape[1], k_pre.shape[2]
+    if scale is None:
+        scale = dh ** -0.5
+    if out is None:
+        out = torch.empty((B, Hq, n_s, dh), dtype=torch.float32, device=q.device)
+    bf = torch.bfloat16
+    args = [_dev(q, bf, "q"), _dev(k_pre, bf, "k_pre"), _dev(v_pre, bf, "v_pre"),
+            _dev(k_suf, bf, "k_suf"), _dev(v_suf, bf, "v_suf"), _dev(out, torch.float32, "out")]
+    _check(lib().bc_request_prefix_attention(*args, B, Hq, Hkv, m, n_s, dh, float(scale), _stream()))
+    return out
+
+
+def is_refresh_step(t, delta):
+    """Refresh schedule of Eq. 5 (host only): True when (t - 1) mod delta == 0."""
+    r = lib().bc_is_refresh_step(t, delta)
+    if r < 0:
+        raise BiCacheError(-1, f"invalid step t={t} or refresh interval delta={delta}")
+    return bool(r)
+
+
+DEEP_MODES = {"refresh": 0, "reuse": 1}
 
 _WEIGHT_KEYS = ("w_qkv", "w_o", "w_gate_up", "w_down", "attn_norm", "ffn_norm")
 
@@ -250,9 +287,32 @@ class Model:
         _check(lib().bc_step_plan(self._h, m, B, n_s, d, rows, pos, kv, C.byref(rh)))
         return list(rows), list(pos), list(kv), rh.value
 
-    def step(self, key, x_suffix, d, out=None):
+    def deep_store_bytes(self, m, B, n_s, d):
+        return int(lib().bc_deep_store_bytes(self._h, m, B, n_s, d))
+
+    def deep_store_offset(self, m, B, n_s, d, layer, part, req, head, pos, dim):
+        return int(lib().bc_deep_store_offset(self._h, m, B, n_s, d, layer, part, req, head, pos, dim))
+
+    def new_deep_store(self, key, B, n_s, d, device="cuda"):
+        """Device memory for the deep store of a batch (None when d = L)."""
+        got = self.lookup(key)
+        if got is None:
+            raise BiCacheError(-2, f"key {key:#x} is not cached")
+        nbytes = self.deep_store_bytes(got[0], B, n_s, d)
+        if nbytes == 0:
+            return None
+        store = torch.empty(nbytes, dtype=torch.uint8, device=device)
+        # the allocator may hand out the address of an earlier, tagged store
+        _check(lib().bc_deep_store_reset(self._h, C.c_void_p(store.data_ptr())))
+        return store
+
+    def step(self, key, x_suffix, d, out=None, deep=None, deep_store=None):
         """Step forward of x_suffix [B, n_s, h] (bf16, device) at reuse depth d.
-        Returns the fp32 suffix rows of the final residual [B, n_s, h]."""
+
+        deep=None runs bc_step_forward; deep="refresh" / "reuse" runs
+        bc_step_forward_deep in that mode with ``deep_store`` (a uint8 device
+        tensor from new_deep_store, or None).  Returns the fp32 suffix rows of
+        the final residual [B, n_s, h]."""
         B, n_s, h = x_suffix.shape
         got = self.lookup(key)
         if got is None:
@@ -264,7 +324,19 @@ class Model:
         ws = self._workspace(wsb, x_suffix.device)
         if out is None:
             out = torch.empty((B, n_s, h), dtype=torch.float32, device=x_suffix.device)
-        _check(lib().bc_step_forward(self._h, C.c_uint64(key), _dev(x_suffix, torch.bfloat16, "x_suffix"),
-                                     B, n_s, d, _dev(out, torch.float32, "out"),
-                                     C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
+        xs = _dev(x_suffix, torch.bfloat16, "x_suffix")
+        o = _dev(out, torch.float32, "out")
+        wsp = C.c_void_p(ws.data_ptr())
+        if deep is None:
+            _check(lib().bc_step_forward(self._h, C.c_uint64(key), xs, B, n_s, d, o, wsp, ws.numel(),
+                                         _stream()))
+            return out
+        if deep not in DEEP_MODES:
+            raise ValueError(f"deep must be one of {sorted(DEEP_MODES)}, got {deep!r}")
+        if deep_store is None:
+            sp, sb = None, 0
+        else:
+            sp, sb = _dev(deep_store, torch.uint8, "deep_store"), deep_store.numel()
+        _check(lib().bc_step_forward_deep(self._h, C.c_uint64(key), xs, B, n_s, d, DEEP_MODES[deep],
+                                          sp, sb, o, wsp, ws.numel(), _stream()))
         return out

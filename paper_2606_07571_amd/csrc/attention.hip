@@ -1,6 +1,8 @@
 // Shared-prefix bidirectional attention on gfx950 (Eq. 2 over [prefix ; own
 // suffix], the shallow-layer form of Eq. 4).  With m = 0 the same kernel is
-// the deep layers' full attention of every request over its own sequence.
+// the deep layers' full attention of every request over its own sequence, and
+// with a per-request prefix (p_sb != 0) it is the deep layers' attention of a
+// step that reuses each request's own prefix K/V (second case of Eq. 5).
 //
 // Work decomposition.  For one KV head g, the query rows of every request b
 // and every query head of g's group are cut into chunks of 32 rows
@@ -12,7 +14,8 @@
 // workgroup and consumed by all 8 waves, whatever request or query head they
 // serve, so one LDS copy of the shared prefix feeds up to 256 query rows of
 // several requests.  A suffix tile is consumed only by the waves of its
-// request.
+// request.  When every request has its own prefix, the prefix tiles join the
+// request's part of the walk: [its prefix tiles ; its suffix tiles].
 //
 // Per wave the scores are computed transposed, S^T = K . Q^T with
 // v_mfma_f32_32x32x16_bf16: a lane then holds 16 scores of ONE query row
@@ -112,15 +115,22 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     }
   }
 
+  // Tile walk: SP tiles shared by every wave (the prefix when one copy
+  // serves all requests), then PR tiles per distinct request of the
+  // workgroup: its own prefix tiles (PP of them, when every request has its
+  // own prefix) followed by its suffix tiles.
   const int TP = cdiv(a.m, KT), TS = cdiv(a.n_s, KT);
-  const int n_tiles = TP + (b_hi - b_lo + 1) * TS;
-  // a wave works on a tile if it is a prefix tile or a suffix tile of its
-  // own request
+  const bool own_pre = a.p_sb != 0;
+  const int SP = own_pre ? 0 : TP, PP = own_pre ? TP : 0, PR = PP + TS;
+  const int n_tiles = SP + (b_hi - b_lo + 1) * PR;
+  // a wave works on a tile if it is shared or belongs to its own request
   auto owns = [&](int t) __attribute__((always_inline)) {
-    return active && t >= 0 && t < n_tiles && (t < TP || b_lo + (t - TP) / TS == b);
+    return active && t >= 0 && t < n_tiles && (t < SP || b_lo + (t - SP) / PR == b);
   };
   auto valid_of = [&](int t) __attribute__((always_inline)) {
-    return t < TP ? min(KT, a.m - t * KT) : min(KT, a.n_s - ((t - TP) % TS) * KT);
+    if (t < SP) return min(KT, a.m - t * KT);
+    const int tt = (t - SP) % PR;
+    return tt < PP ? min(KT, a.m - tt * KT) : min(KT, a.n_s - (tt - PP) * KT);
   };
 
   // this thread's share of a fill: K chunks q = tid + 512p (row q / KCH,
@@ -146,16 +156,23 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   auto fetch = [&](int t) __attribute__((always_inline)) {
     const bf16 *kb = (const bf16*)a.kp, *vb = (const bf16*)a.vp;
     int bytes = 0;
-    if (t < TP) {
+    if (t < SP) {
       kb += g * a.p_sh + (long)t * KT * DH;
       vb += g * a.p_sh + (long)t * KT * DH;
       bytes = min(KT, a.m - t * KT) * DH * 2;
     } else if (t < n_tiles) {
-      const int u = t - TP, rb = b_lo + u / TS, tt = u % TS;
-      const long off = rb * a.s_sb + g * a.s_sh + (long)tt * KT * DH;
-      kb = (const bf16*)a.ks + off;
-      vb = (const bf16*)a.vs + off;
-      bytes = min(KT, a.n_s - tt * KT) * DH * 2;
+      const int u = t - SP, rb = b_lo + u / PR, tt = u % PR;
+      if (tt < PP) {
+        const long off = rb * a.p_sb + g * a.p_sh + (long)tt * KT * DH;
+        kb += off;
+        vb += off;
+        bytes = min(KT, a.m - tt * KT) * DH * 2;
+      } else {
+        const long off = rb * a.s_sb + g * a.s_sh + (long)(tt - PP) * KT * DH;
+        kb = (const bf16*)a.ks + off;
+        vb = (const bf16*)a.vs + off;
+        bytes = min(KT, a.n_s - (tt - PP) * KT) * DH * 2;
+      }
     }
     const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kb), (short)0, bytes, RSRC_W3);
     const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vb), (short)0, bytes, RSRC_W3);

@@ -34,16 +34,17 @@ hipError_t gemm_qkv_rope(const void* A, int lda, const void* W, int ldw, int M, 
                          int Hkv, int dh, int n_seq, int pos0, const float* cos_t,
                          const float* sin_t, const QkvOut& out, hipStream_t s);
 
-// ----- attention: one launch of shared-prefix bidirectional attention.
+// ----- attention: one launch of prefix + suffix bidirectional attention.
 // Prefix K/V [Hkv][m][dh] (head stride p_sh elements, rows dh apart) are shared
-// by every request; suffix K/V are per request.  m may be 0 (plain full
-// attention of each request over its own n_s keys).
+// by every request when p_sb == 0; otherwise request b's prefix starts p_sb
+// elements after request b-1's.  Suffix K/V are per request.  m may be 0
+// (plain full attention of each request over its own n_s keys).
 struct AttnArgs {
   const void* q;
   long q_sb, q_sh, q_sr;
   const void* kp;
   const void* vp;
-  long p_sh;
+  long p_sb, p_sh;
   const void* ks;
   const void* vs;
   long s_sb, s_sh, s_sr;

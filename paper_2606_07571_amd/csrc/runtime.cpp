@@ -1,6 +1,8 @@
 // Host runtime and C ABI of libbicache.so: argument validation, the KV store H
-// with FIFO eviction, cache-entry and workspace layouts, and the layer loops
-// of populate (prefix-only forward) and of the step at reuse depth d.
+// with FIFO eviction, cache-entry, deep-store and workspace layouts, and the
+// layer loops of populate (prefix-only forward), of the step at reuse depth d
+// (refresh case of Eq. 5 for the deep layers) and of the reuse step (second
+// case of Eq. 5).
 //
 // Every device buffer is the caller's; this file only carves caller-provided
 // workspace into sub-buffers and enqueues kernels on the caller's stream.
@@ -12,6 +14,7 @@
 #include <cstdint>
 #include <new>
 #include <string>
+#include <unordered_map>
 #include <vector>
 
 #include "../../include/bicache.h"
@@ -30,11 +33,19 @@ struct Profiler {
   std::vector<Rec> recs;
 };
 
+// What the last refresh step wrote into a deep store (keyed by its address):
+// a reuse step must match it.
+struct DeepTag {
+  uint64_t key;
+  int m, B, n_s, d;
+};
+
 struct bc_model {
   bc_model_config cfg;
   std::vector<bc_layer_weights> layers;
   bc::CacheTable table;
   Profiler prof;
+  std::unordered_map<uintptr_t, DeepTag> deep_tags;
   bc_model(const bc_model_config& c, const bc_layer_weights* l, int cap)
       : cfg(c), layers(l, l + c.n_layers), table(cap) {}
   ~bc_model() {
@@ -117,6 +128,25 @@ EntryLayout entry_layout(const bc_model_config& c, int m, int Lc) {
   return e;
 }
 
+// Deep store of a batch: for each deep layer l in [d, L), K then V, each
+// [B][Hkv][N][dh] bf16 with N = m + n_s (the refresh step's K/V of every row;
+// reuse steps read rows 0..m-1).  Every block is a multiple of 256 bytes.
+struct DeepLayout {
+  size_t part = 0;  // bytes of one layer's K or V block
+  size_t total = 0;
+  long sb = 0, sh = 0;  // request and head strides (elements)
+};
+
+DeepLayout deep_layout(const bc_model_config& c, int m, int B, int n_s, int d) {
+  DeepLayout dl;
+  const long N = (long)m + n_s;
+  dl.sh = N * c.head_dim;
+  dl.sb = (long)c.n_kv_heads * dl.sh;
+  dl.part = (size_t)B * dl.sb * 2;
+  dl.total = (size_t)(c.n_layers - d) * 2 * dl.part;
+  return dl;
+}
+
 bool config_ok(const bc_model_config& c, std::string* why) {
   char buf[256];
   auto bad = [&](const char* s) {
@@ -171,8 +201,9 @@ hipError_t prof_mark(bc_model* mdl, int kind, hipStream_t s, size_t* idx) {
 // residual R.  Row r is token t = r % n_seq of request r / n_seq at RoPE
 // position pos0 + t.  The layer's own K/V are written to k_dst/v_dst
 // (element (req, head, t, dim) at req*kv_sb + head*kv_sh + t*dh + dim).
-// Attention of every request runs over [kp/vp (m_pre shared prefix rows, may be
-// 0) ; its own n_seq keys].
+// Attention of every request runs over [kp/vp (m_pre prefix rows, may be 0) ;
+// its own n_seq keys]; the prefix is shared by all requests when kp_sb == 0,
+// else request r's starts at kp + r*kp_sb (head stride kp_sh, 0 = m_pre*dh).
 struct LayerCall {
   float* R;
   int n_req, n_seq, pos0;
@@ -182,6 +213,7 @@ struct LayerCall {
   void* k_dst;
   void* v_dst;
   long kv_sb, kv_sh;
+  long kp_sb = 0, kp_sh = 0;
 };
 
 bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const Plan& p,
@@ -211,7 +243,8 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
   a.q_sr = dh;
   a.kp = lc.kp;
   a.vp = lc.vp;
-  a.p_sh = (long)lc.m_pre * dh;
+  a.p_sb = lc.kp_sb;
+  a.p_sh = lc.kp_sh ? lc.kp_sh : (long)lc.m_pre * dh;
   a.ks = lc.k_dst;
   a.vs = lc.v_dst;
   a.s_sb = lc.kv_sb;
@@ -258,6 +291,137 @@ bool step_shape_ok(const bc_model_config& c, int m, int B, int n_s, int d, std::
     return false;
   }
   return true;
+}
+
+
+// Both kinds of step.  mode BC_DEEP_REFRESH: layers l < d suffix-only over
+// KV$_l, layers l >= d recompute the prefix from H$_d (their K/V of every row
+// go to `store` when it is non-null, else to the workspace).  BC_DEEP_REUSE:
+// every layer suffix-only, deep layers over the request's prefix rows in
+// `store`.
+bc_status step_impl(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s, int d,
+                    int mode, void* store, size_t store_bytes, float* out, void* workspace,
+                    size_t ws_bytes, void* stream) {
+  if (!model || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (mode != BC_DEEP_REFRESH && mode != BC_DEEP_REUSE) return fail(BC_E_INVALID, "unknown deep mode %d", mode);
+  const bc_model_config& c = model->cfg;
+  const int L = c.n_layers;
+  const bc::CacheEntry* ent = model->table.find(key);
+  if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
+  const int m = ent->m;
+  std::string why;
+  if (!step_shape_ok(c, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  if (d > ent->n_layers)
+    return fail(BC_E_INVALID, "reuse depth d=%d exceeds the %d cached layers of this prefix", d, ent->n_layers);
+  const long N = (long)m + n_s;
+  const bool full = mode == BC_DEEP_REFRESH && d < L;  // deep layers run over all N rows
+  const long rows_max = (long)B * (full ? N : n_s);
+  const Plan p = make_plan(c, rows_max, N, true, full ? (long)B * N : 0);
+  if (ws_bytes < p.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, p.total);
+  if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
+  const DeepLayout dl = deep_layout(c, m, B, n_s, d);
+  const bool use_store = d < L && (mode == BC_DEEP_REUSE || store);
+  if (use_store) {
+    if (!store) return fail(BC_E_INVALID, "a reuse step at d=%d < L needs the deep store", d);
+    if (store_bytes < dl.total) return fail(BC_E_INVALID, "deep store %zu < required %zu", store_bytes, dl.total);
+    if ((uintptr_t)store % kAlign) return fail(BC_E_INVALID, "deep store must be 256-byte aligned");
+  }
+  if (use_store && mode == BC_DEEP_REUSE) {
+    auto it = model->deep_tags.find((uintptr_t)store);
+    if (it == model->deep_tags.end())
+      return fail(BC_E_STATE, "no refresh step has written this deep store");
+    const DeepTag& tg = it->second;
+    if (tg.key != key || tg.m != m || tg.B != B || tg.n_s != n_s || tg.d != d)
+      return fail(BC_E_STATE,
+                  "deep store was refreshed for key %016llx m=%d B=%d n_s=%d d=%d, not key %016llx m=%d B=%d n_s=%d d=%d",
+                  (unsigned long long)tg.key, tg.m, tg.B, tg.n_s, tg.d, (unsigned long long)key, m, B, n_s, d);
+  }
+
+  hipStream_t s = (hipStream_t)stream;
+  char* ws = (char*)workspace;
+  char* st_mem = (char*)store;
+  const char* cm = (const char*)ent->mem;
+  const EntryLayout e = entry_layout(c, m, ent->n_layers);
+  const int dh = c.head_dim, Hkv = c.n_kv_heads;
+  auto deep_k = [&](int l) { return st_mem + (size_t)(2 * (l - d)) * dl.part; };
+  auto deep_v = [&](int l) { return st_mem + (size_t)(2 * (l - d) + 1) * dl.part; };
+
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), (int)N, dh, c.rope_theta, s));
+  // suffix-only residual, kept in `out`
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_suffix, out, (long)B * n_s * c.hidden, s));
+  const int n_suffix_layers = full ? d : L;
+  for (int l = 0; l < n_suffix_layers; ++l) {
+    LayerCall lc{out, B, n_s, m, nullptr, nullptr, m,
+                 ws + p.k, ws + p.v, (long)Hkv * n_s * dh, (long)n_s * dh};
+    if (l < d) {  // Eq. 4: the shared KV$_l
+      lc.kp = cm + (size_t)(2 * l) * e.kv_layer;
+      lc.vp = cm + (size_t)(2 * l + 1) * e.kv_layer;
+    } else {      // second case of Eq. 5: this request's prefix K/V of the last refresh
+      lc.kp = deep_k(l);
+      lc.vp = deep_v(l);
+      lc.kp_sb = dl.sb;
+      lc.kp_sh = dl.sh;
+    }
+    bc_status st = run_layer(model, l, lc, ws, p, s);
+    if (st != BC_OK) return st;
+  }
+  if (full) {
+    float* R = (float*)(ws + p.R);
+    const float* hd = (const float*)(cm + e.h_off + (size_t)d * e.h_layer);
+    BC_LAUNCH(model, BC_K_OTHER, s, bc::build_full_residual(hd, out, R, B, m, n_s, c.hidden, s));
+    for (int l = d; l < L; ++l) {
+      void* kd = use_store ? (void*)deep_k(l) : (void*)(ws + p.k);
+      void* vd = use_store ? (void*)deep_v(l) : (void*)(ws + p.v);
+      LayerCall lc{R, B, (int)N, 0, nullptr, nullptr, 0, kd, vd, dl.sb, dl.sh};
+      bc_status st = run_layer(model, l, lc, ws, p, s);
+      if (st != BC_OK) return st;
+    }
+    BC_LAUNCH(model, BC_K_OTHER, s, bc::gather_suffix(R, out, B, m, n_s, c.hidden, s));
+    if (use_store) model->deep_tags[(uintptr_t)store] = DeepTag{key, m, B, n_s, d};
+  }
+  return ok();
+}
+
+
+bc_status prefix_attention(const void* q, const void* k_pre, const void* v_pre, long pre_sb,
+                           const void* k_suf, const void* v_suf, float* out, int B, int Hq,
+                           int Hkv, int m, int n_s, int dh, float scale, void* stream) {
+  if (!q || !k_suf || !v_suf || !out || (m > 0 && (!k_pre || !v_pre)))
+    return fail(BC_E_INVALID, "null argument");
+  if (B < 1 || n_s < 1 || m < 0) return fail(BC_E_INVALID, "B, n_s >= 1 and m >= 0 required");
+  if (dh != 64 && dh != 128) return fail(BC_E_INVALID, "dh must be 64 or 128 (got %d)", dh);
+  if (Hq < 1 || Hkv < 1 || Hq % Hkv) return fail(BC_E_INVALID, "Hq must be a positive multiple of Hkv");
+  if ((long)B * Hq * ((n_s + 31) / 32) > INT_MAX / 2 || (long)m * dh > INT_MAX / 2 ||
+      (long)n_s * dh > INT_MAX / 2)
+    return fail(BC_E_CAPACITY, "attention problem too large");
+  bc::AttnArgs a{};
+  a.q = q;
+  a.q_sb = (long)Hq * n_s * dh;
+  a.q_sh = (long)n_s * dh;
+  a.q_sr = dh;
+  a.kp = k_pre;
+  a.vp = v_pre;
+  a.p_sb = m > 0 ? pre_sb : 0;
+  a.p_sh = (long)m * dh;
+  a.ks = k_suf;
+  a.vs = v_suf;
+  a.s_sb = (long)Hkv * n_s * dh;
+  a.s_sh = (long)n_s * dh;
+  a.s_sr = dh;
+  a.out = out;
+  a.o_sb = (long)Hq * n_s * dh;
+  a.o_sh = (long)n_s * dh;
+  a.o_sr = dh;
+  a.B = B;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.m = m;
+  a.n_s = n_s;
+  a.dh = dh;
+  a.scale = scale;
+  a.out_f32 = 1;
+  BC_HIP(bc::attention(a, (hipStream_t)stream));
+  return ok();
 }
 
 }  // namespace
@@ -433,53 +597,51 @@ bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int*
   return ok();
 }
 
+
 bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
                           int d, float* out, void* workspace, size_t ws_bytes, void* stream) {
-  if (!model || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
-  const bc_model_config& c = model->cfg;
-  const int L = c.n_layers;
-  const bc::CacheEntry* ent = model->table.find(key);
-  if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
-  const int m = ent->m;
+  return step_impl(model, key, x_suffix, B, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out, workspace,
+                   ws_bytes, stream);
+}
+
+size_t bc_deep_store_bytes(const bc_model* model, int m, int B, int n_s, int d) {
+  if (!model) return 0;
   std::string why;
-  if (!step_shape_ok(c, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
-  if (d > ent->n_layers)
-    return fail(BC_E_INVALID, "reuse depth d=%d exceeds the %d cached layers of this prefix", d, ent->n_layers);
-  const long N = (long)m + n_s;
-  const long rows_max = (long)B * (d < L ? N : n_s);
-  const Plan p = make_plan(c, rows_max, N, true, d < L ? (long)B * N : 0);
-  if (ws_bytes < p.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, p.total);
-  if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
+  if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return 0;
+  return deep_layout(model->cfg, m, B, n_s, d).total;
+}
 
-  hipStream_t s = (hipStream_t)stream;
-  char* ws = (char*)workspace;
-  const char* cm = (const char*)ent->mem;
-  const EntryLayout e = entry_layout(c, m, ent->n_layers);
-  const int dh = c.head_dim, Hkv = c.n_kv_heads;
+size_t bc_deep_store_offset(const bc_model* model, int m, int B, int n_s, int d, int layer,
+                            int part, int req, int head, int pos, int dim) {
+  const size_t bad = (size_t)-1;
+  if (!model) return bad;
+  const bc_model_config& c = model->cfg;
+  std::string why;
+  if (!step_shape_ok(c, m, B, n_s, d, &why)) return bad;
+  if (layer < d || layer >= c.n_layers || part < 0 || part > 1 || req < 0 || req >= B ||
+      head < 0 || head >= c.n_kv_heads || pos < 0 || pos >= m + n_s || dim < 0 || dim >= c.head_dim)
+    return bad;
+  const DeepLayout dl = deep_layout(c, m, B, n_s, d);
+  return (size_t)(2 * (layer - d) + part) * dl.part +
+         ((size_t)req * dl.sb + (size_t)head * dl.sh + (size_t)pos * c.head_dim + dim) * 2;
+}
 
-  BC_LAUNCH(model, BC_K_OTHER, s, bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), (int)N, dh, c.rope_theta, s));
-  // shallow residual: the suffix rows only, kept in `out`
-  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_suffix, out, (long)B * n_s * c.hidden, s));
-  for (int l = 0; l < d; ++l) {
-    LayerCall lc{out, B, n_s, m,
-                 cm + (size_t)(2 * l) * e.kv_layer, cm + (size_t)(2 * l + 1) * e.kv_layer, m,
-                 ws + p.k, ws + p.v, (long)Hkv * n_s * dh, (long)n_s * dh};
-    bc_status st = run_layer(model, l, lc, ws, p, s);
-    if (st != BC_OK) return st;
-  }
-  if (d < L) {
-    float* R = (float*)(ws + p.R);
-    const float* hd = (const float*)(cm + e.h_off + (size_t)d * e.h_layer);
-    BC_LAUNCH(model, BC_K_OTHER, s, bc::build_full_residual(hd, out, R, B, m, n_s, c.hidden, s));
-    for (int l = d; l < L; ++l) {
-      LayerCall lc{R, B, (int)N, 0, nullptr, nullptr, 0,
-                   ws + p.k, ws + p.v, (long)Hkv * N * dh, N * dh};
-      bc_status st = run_layer(model, l, lc, ws, p, s);
-      if (st != BC_OK) return st;
-    }
-    BC_LAUNCH(model, BC_K_OTHER, s, bc::gather_suffix(R, out, B, m, n_s, c.hidden, s));
-  }
+bc_status bc_deep_store_reset(bc_model* model, const void* deep_store) {
+  if (!model) return fail(BC_E_INVALID, "null model");
+  model->deep_tags.erase((uintptr_t)deep_store);
   return ok();
+}
+
+int bc_is_refresh_step(int t, int delta) {
+  if (t < 1 || delta < 1) return -1;
+  return (t - 1) % delta == 0 ? 1 : 0;
+}
+
+bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suffix, int B,
+                               int n_s, int d, int mode, void* deep_store, size_t store_bytes,
+                               float* out, void* workspace, size_t ws_bytes, void* stream) {
+  return step_impl(model, key, x_suffix, B, n_s, d, mode, deep_store, store_bytes, out, workspace,
+                   ws_bytes, stream);
 }
 
 bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) {
@@ -512,45 +674,21 @@ bc_status bc_profile_end(bc_model* model, double* ms, int* launches) {
   return ok();
 }
 
+
 bc_status bc_shared_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
                                      const void* k_suf, const void* v_suf, float* out, int B,
                                      int Hq, int Hkv, int m, int n_s, int dh, float scale,
                                      void* stream) {
-  if (!q || !k_suf || !v_suf || !out || (m > 0 && (!k_pre || !v_pre)))
-    return fail(BC_E_INVALID, "null argument");
-  if (B < 1 || n_s < 1 || m < 0) return fail(BC_E_INVALID, "B, n_s >= 1 and m >= 0 required");
-  if (dh != 64 && dh != 128) return fail(BC_E_INVALID, "dh must be 64 or 128 (got %d)", dh);
-  if (Hq < 1 || Hkv < 1 || Hq % Hkv) return fail(BC_E_INVALID, "Hq must be a positive multiple of Hkv");
-  if ((long)B * Hq * ((n_s + 31) / 32) > INT_MAX / 2 || (long)m * dh > INT_MAX / 2 ||
-      (long)n_s * dh > INT_MAX / 2)
-    return fail(BC_E_CAPACITY, "attention problem too large");
-  bc::AttnArgs a{};
-  a.q = q;
-  a.q_sb = (long)Hq * n_s * dh;
-  a.q_sh = (long)n_s * dh;
-  a.q_sr = dh;
-  a.kp = k_pre;
-  a.vp = v_pre;
-  a.p_sh = (long)m * dh;
-  a.ks = k_suf;
-  a.vs = v_suf;
-  a.s_sb = (long)Hkv * n_s * dh;
-  a.s_sh = (long)n_s * dh;
-  a.s_sr = dh;
-  a.out = out;
-  a.o_sb = (long)Hq * n_s * dh;
-  a.o_sh = (long)n_s * dh;
-  a.o_sr = dh;
-  a.B = B;
-  a.Hq = Hq;
-  a.Hkv = Hkv;
-  a.m = m;
-  a.n_s = n_s;
-  a.dh = dh;
-  a.scale = scale;
-  a.out_f32 = 1;
-  BC_HIP(bc::attention(a, (hipStream_t)stream));
-  return ok();
+  return prefix_attention(q, k_pre, v_pre, 0, k_suf, v_suf, out, B, Hq, Hkv, m, n_s, dh, scale,
+                          stream);
+}
+
+bc_status bc_request_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
+                                      const void* k_suf, const void* v_suf, float* out, int B,
+                                      int Hq, int Hkv, int m, int n_s, int dh, float scale,
+                                      void* stream) {
+  return prefix_attention(q, k_pre, v_pre, (long)Hkv * m * dh, k_suf, v_suf, out, B, Hq, Hkv, m,
+                          n_s, dh, scale, stream);
 }
 
 }  // extern "C"

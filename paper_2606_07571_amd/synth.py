@@ -128,3 +128,27 @@ def to_f64(t):
 
 def weights_f64(layers):
     return [{k: to_f64(v) for k, v in lw.items()} for lw in layers]
+
+
+def denoise_inputs(cfg, T, B, n_s, n_gen, per_step, seed_base, device="cpu"):
+    """Suffix inputs of T consecutive denoising steps, [T, B, n_s, h] bf16.
+
+    A request's suffix is its own prompt rows (n_s - n_gen rows, N(0, 1)) then
+    n_gen generation slots that start as one shared [MASK] embedding row; each
+    step fills per_step more slots (left to right) with fresh N(0, 1) rows, as
+    the tokens denoised at the previous step enter the input.
+    """
+    h = cfg["hidden"]
+    assert 0 <= n_gen <= n_s
+    x = gaussian((B, n_s, h), seed_base + 0).float()
+    mask_row = gaussian((h,), seed_base + 1).float()
+    x[:, n_s - n_gen:] = mask_row
+    fresh = gaussian((T, B, n_gen, h), seed_base + 2).float()
+    out = []
+    for t in range(T):
+        out.append(x.clone())
+        lo = n_s - n_gen + t * per_step
+        hi = min(n_s, lo + per_step)
+        if lo < hi:
+            x[:, lo:hi] = fresh[t, :, :hi - lo]
+    return torch.stack(out).to(torch.bfloat16).to(device)

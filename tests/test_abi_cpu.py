@@ -158,6 +158,68 @@ def test_entry_point_validation_without_device_work():
     L.bc_model_destroy(h)
 
 
+def test_refresh_schedule_matches_oracle():
+    from oracle.transformer import is_refresh_step
+    for delta in (1, 2, 3, 16, 64):
+        for t in range(1, 200):
+            assert bc.is_refresh_step(t, delta) == is_refresh_step(t, delta)
+    L = bc.lib()
+    assert L.bc_is_refresh_step(0, 16) == -1 and L.bc_is_refresh_step(1, 0) == -1
+    assert L.bc_is_refresh_step(-5, 3) == -1
+    with pytest.raises(bc.BiCacheError):
+        bc.is_refresh_step(0, 16)
+
+
+def test_deep_store_layout_offsets():
+    st, h = _model()
+    L = bc.lib()
+    m, B, n_s = 129, 3, 65
+    Hkv, dh, nl = 2, 64, 3
+    N = m + n_s
+    for d in range(nl + 1):
+        part = B * Hkv * N * dh * 2
+        assert L.bc_deep_store_bytes(h, m, B, n_s, d) == (nl - d) * 2 * part
+        assert part % 256 == 0
+        for (layer, pt, req, head, pos, dim) in [(d, 0, 0, 0, 0, 0), (nl - 1, 1, B - 1, Hkv - 1, N - 1, dh - 1),
+                                                 (d, 1, 1, 0, m, 3)]:
+            off = L.bc_deep_store_offset(h, m, B, n_s, d, layer, pt, req, head, pos, dim)
+            if d == nl:
+                assert off == (1 << 64) - 1
+                continue
+            exp = (2 * (layer - d) + pt) * part + (((req * Hkv + head) * N + pos) * dh + dim) * 2
+            assert off == exp
+    bad = (1 << 64) - 1
+    d = 1
+    assert L.bc_deep_store_offset(h, m, B, n_s, d, 0, 0, 0, 0, 0, 0) == bad      # shallow layer
+    assert L.bc_deep_store_offset(h, m, B, n_s, d, 3, 0, 0, 0, 0, 0) == bad      # layer >= L
+    assert L.bc_deep_store_offset(h, m, B, n_s, d, 1, 2, 0, 0, 0, 0) == bad      # no such part
+    assert L.bc_deep_store_offset(h, m, B, n_s, d, 1, 0, B, 0, 0, 0) == bad      # req >= B
+    assert L.bc_deep_store_offset(h, m, B, n_s, d, 1, 0, 0, 0, N, 0) == bad      # pos >= N
+    assert L.bc_deep_store_bytes(h, m, B, n_s, 4) == 0
+    assert L.bc_deep_store_bytes(h, 0, B, n_s, 1) == 0
+    # the last element ends the store
+    last = L.bc_deep_store_offset(h, m, B, n_s, 0, nl - 1, 1, B - 1, Hkv - 1, N - 1, dh - 1)
+    assert last + 2 == L.bc_deep_store_bytes(h, m, B, n_s, 0)
+    L.bc_model_destroy(h)
+
+
+def test_deep_step_validation_without_device_work():
+    st, h = _model()
+    L = bc.lib()
+    big = 1 << 40
+    S = L.bc_step_forward_deep
+    # miss first, then mode checks never reach the device
+    assert S(h, 1, FAKE, 2, 4, 1, 1, FAKE, big, FAKE, FAKE, big, None) == -2
+    assert S(h, 1, FAKE, 2, 4, 1, 7, FAKE, big, FAKE, FAKE, big, None) == -1
+    assert "deep mode" in L.bc_last_error().decode()
+    assert S(h, 1, None, 2, 4, 1, 0, FAKE, big, FAKE, FAKE, big, None) == -1
+    assert L.bc_deep_store_reset(h, FAKE) == 0 and L.bc_deep_store_reset(None, FAKE) == -1
+    A = L.bc_request_prefix_attention
+    assert A(FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 8, 4, 96, 0.1, None) == -1   # dh
+    assert A(FAKE, None, FAKE, FAKE, FAKE, FAKE, 2, 4, 4, 8, 4, 64, 0.1, None) == -1   # null prefix, m > 0
+    L.bc_model_destroy(h)
+
+
 # ------------------------------------------------------------ FIFO bookkeeping
 
 @pytest.fixture(scope="module")
