@@ -9,6 +9,9 @@
   a request's output rows are bit-identical whether it runs alone or in the
   batch, reversing the batch reverses the outputs bit for bit, and a repeated
   step reproduces its output exactly.
+* Deep-layer reuse at the full C3 size (d = 8): a reuse step right after a
+  refresh reproduces it bit for bit (1536 is a whole number of key tiles),
+  and a request refreshed and reused alone gives its batch rows.
 * The C4 populate (prefix 8192, 8 layers of the C3 shape): the first layer's
   cached K/V at sampled positions against the oracle, computed row by row,
   and the first cached residual, which is the exact widening of the input.
@@ -136,3 +139,44 @@ def test_c4_populate_first_layer_sampled():
         assert_close_bf16_store(v_got, v_ref, "C4 KV$ layer 0 V (sampled rows)")
     finally:
         model.close()
+
+
+def test_c3_full_size_deep_reuse(c3_full):
+    """Deep-layer reuse (second case of Eq. 5) at the full C3 size, d = 8.
+    The prefix (1536) is a whole number of 64-key tiles, so a reuse step right
+    after a refresh with the same input walks the same key tiles in the same
+    order and reproduces the refresh output bit for bit; a request refreshed
+    and reused on its own gives its batch rows bit for bit."""
+    cfg, model, key, xs = c3_full
+    B, n_s = xs.shape[0], xs.shape[1]
+    d = 8
+    store = model.new_deep_store(key, B, n_s, d)
+    say(f"C3 full: refresh with deep store d={d} ({store.numel() / 2**30:.1f} GiB)")
+    ref = model.step(key, xs, d, deep="refresh", deep_store=store)
+    say("C3 full: reuse step, same input")
+    got = model.step(key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.isfinite(got).all()
+    assert torch.equal(got, ref), "reuse right after refresh differs from the refresh"
+    # a changed suffix: the reuse step sees the new suffix, the stale prefix K/V
+    xs2 = xs.clone()
+    xs2[:, -16:] = xs.flip(0)[:, -16:]
+    say("C3 full: reuse step, changed suffix")
+    got2 = model.step(key, xs2, d, deep="reuse", deep_store=store)
+    fresh2 = model.step(key, xs2, d)
+    torch.cuda.synchronize()
+    assert torch.isfinite(got2).all()
+    assert not torch.equal(got2, got)
+    # the last request alone: refresh and reuse in a store of its own
+    b = B - 1
+    one_store = model.new_deep_store(key, 1, n_s, d)
+    say("C3 full: last request alone")
+    model.step(key, xs[b:b + 1].contiguous(), d, deep="refresh", deep_store=one_store)
+    one = model.step(key, xs2[b:b + 1].contiguous(), d, deep="reuse", deep_store=one_store)
+    torch.cuda.synchronize()
+    assert torch.equal(one[0], got2[b])
+    diff = (got2 - fresh2).abs()
+    say(f"  reuse vs fresh recompute with a changed suffix: max {diff.max().item():.3e} "
+        f"mean {diff.mean().item():.3e}")
+    del store, one_store
+    torch.cuda.empty_cache()
