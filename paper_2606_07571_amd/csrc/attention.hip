@@ -115,23 +115,54 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     }
   }
 
-  // Tile walk: SP tiles shared by every wave (the prefix when one copy
-  // serves all requests), then PR tiles per distinct request of the
-  // workgroup: its own prefix tiles (PP of them, when every request has its
-  // own prefix) followed by its suffix tiles.
+  // Tile walk: the shared prefix (when one copy serves all requests), then
+  // for each distinct request of the workgroup its own prefix (when every
+  // request has one) and its suffix.  The walk is a cursor over these
+  // segments: the fetch of a tile reads the cursor and advances it by one
+  // tile, a few scalar operations, with a segment change only at segment
+  // ends.  Fetches happen in tile order, once per tile.
   const int TP = cdiv(a.m, KT), TS = cdiv(a.n_s, KT);
   const bool own_pre = a.p_sb != 0;
-  const int SP = own_pre ? 0 : TP, PP = own_pre ? TP : 0, PR = PP + TS;
+  const int SP = own_pre ? 0 : TP, PR = (own_pre ? TP : 0) + TS;
   const int n_tiles = SP + (b_hi - b_lo + 1) * PR;
-  // a wave works on a tile if it is shared or belongs to its own request
-  auto owns = [&](int t) __attribute__((always_inline)) {
-    return active && t >= 0 && t < n_tiles && (t < SP || b_lo + (t - SP) / PR == b);
+  const bf16* const kp0 = (const bf16*)a.kp + g * a.p_sh;
+  const bf16* const vp0 = (const bf16*)a.vp + g * a.p_sh;
+  const bf16* const ks0 = (const bf16*)a.ks + g * a.s_sh;
+  const bf16* const vs0 = (const bf16*)a.vs + g * a.s_sh;
+  const bf16* wk = kp0;   // first key row of the next tile to fetch
+  const bf16* wv = vp0;
+  int w_left = 0;         // key rows from there to the end of its segment
+  int w_req = 0;          // request of the segment, -1 for the shared prefix
+  int w_phase = 0;        // 0 shared prefix, 1 own prefix, 2 suffix
+  // enter segment (phase, req), skipping empty ones; past the last request
+  // the walk stays at the end (w_left = 0: empty tiles)
+  auto enter = [&](int phase, int req) __attribute__((always_inline)) {
+    for (;;) {
+      if (req > b_hi) { w_left = 0; w_req = req; w_phase = 2; return; }
+      if (phase == 0) {
+        if (SP > 0) { wk = kp0; wv = vp0; w_left = a.m; w_req = -1; w_phase = 0; return; }
+        phase = own_pre ? 1 : 2;
+        req = b_lo;
+      } else if (phase == 1) {
+        if (a.m > 0) {
+          wk = kp0 + req * a.p_sb;
+          wv = vp0 + req * a.p_sb;
+          w_left = a.m; w_req = req; w_phase = 1;
+          return;
+        }
+        phase = 2;
+      } else {
+        wk = ks0 + req * a.s_sb;
+        wv = vs0 + req * a.s_sb;
+        w_left = a.n_s; w_req = req; w_phase = 2;
+        return;
+      }
+    }
   };
-  auto valid_of = [&](int t) __attribute__((always_inline)) {
-    if (t < SP) return min(KT, a.m - t * KT);
-    const int tt = (t - SP) % PR;
-    return tt < PP ? min(KT, a.m - tt * KT) : min(KT, a.n_s - (tt - PP) * KT);
-  };
+  enter(0, b_lo);
+  // valid keys of each fetched tile for this wave (0 for tiles of another
+  // request and past the end), queued from fetch to use: tiles u..u+3
+  int nvq0 = 0, nvq1 = 0, nvq2 = 0, nvq3 = 0;
 
   // this thread's share of a fill: K chunks q = tid + 512p (row q / KCH,
   // chunk q % KCH); V key pair kp = tid % 32 of dim group tid / 32
@@ -143,7 +174,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     ks_off[p] = r * KROW + kc * 8;                     // elements in the LDS K tile
   }
   const int kp = tid & 31, dgl = tid >> 5;
-  const bool v_ok = dgl < KCH;
+  const bool v_ok = KCH * 32 >= 512 || dgl < KCH;   // always, for dh 128
   const int dg = v_ok ? dgl : 0;
   const int vg_off = (2 * kp * DH + dg * 8) * 2;
   // key 2kp sits at position chunk*8 + elem of its V^T row, with the 16 keys
@@ -152,30 +183,23 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   const int vs_off = KTILE + dg * 8 * VROW + vpos;
 
   u32x4 kreg[K_PER], vreg[2];
-  // tiles past the end get an empty descriptor: their loads return zeros
-  auto fetch = [&](int t) __attribute__((always_inline)) {
-    const bf16 *kb = (const bf16*)a.kp, *vb = (const bf16*)a.vp;
-    int bytes = 0;
-    if (t < SP) {
-      kb += g * a.p_sh + (long)t * KT * DH;
-      vb += g * a.p_sh + (long)t * KT * DH;
-      bytes = min(KT, a.m - t * KT) * DH * 2;
-    } else if (t < n_tiles) {
-      const int u = t - SP, rb = b_lo + u / PR, tt = u % PR;
-      if (tt < PP) {
-        const long off = rb * a.p_sb + g * a.p_sh + (long)tt * KT * DH;
-        kb += off;
-        vb += off;
-        bytes = min(KT, a.m - tt * KT) * DH * 2;
-      } else {
-        const long off = rb * a.s_sb + g * a.s_sh + (long)(tt - PP) * KT * DH;
-        kb = (const bf16*)a.ks + off;
-        vb = (const bf16*)a.vs + off;
-        bytes = min(KT, a.n_s - (tt - PP) * KT) * DH * 2;
-      }
+  // fetch of the tile at the cursor, which then moves on; tiles past the end
+  // get an empty descriptor, so their loads return zeros
+  auto fetch = [&]() __attribute__((always_inline)) {
+    const int nv = min(KT, w_left);
+    const int bytes = nv * DH * 2;
+    nvq3 = (active && (w_req < 0 || w_req == b)) ? nv : 0;
+    const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wk), (short)0, bytes, RSRC_W3);
+    const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wv), (short)0, bytes, RSRC_W3);
+    if (w_left > KT) {
+      wk += KT * DH;
+      wv += KT * DH;
+      w_left -= KT;
+    } else if (w_req <= b_hi) {
+      if (w_phase == 0) enter(own_pre ? 1 : 2, b_lo);
+      else if (w_phase == 1) enter(2, w_req);
+      else enter(own_pre ? 1 : 2, w_req + 1);
     }
-    const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(kb), (short)0, bytes, RSRC_W3);
-    const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(vb), (short)0, bytes, RSRC_W3);
 #pragma unroll
     for (int p = 0; p < K_PER; ++p) kreg[p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
     vreg[0] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off, 0, 0);
@@ -257,6 +281,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   // that moves O and the row sum to the new max (1 when it does not move).
   // The first tile of a row always moves it (m starts at -inf, kept finite
   // so that fully masked tiles give exp2(-inf) = 0).
+  bool moved = false;   // wave-uniform: the last new_max moved the running max
   auto new_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
     float mx = -INFINITY;
 #pragma unroll
@@ -265,6 +290,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[kb][e]);
     mx = half_max(mx) * sl2;
     const bool move = __builtin_amdgcn_ballot_w64(mx > m_run + 8.f) != 0;
+    moved = move;
     const float m_new = move ? fmaxf(m_run, mx) : m_run;
     const float alpha = __builtin_amdgcn_exp2f(m_run - m_new);
     m_run = m_new;
@@ -308,7 +334,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       __attribute__((always_inline)) {
     constexpr bool PV = decltype(has_pv)::value;
     float lt[4] = {0.f, 0.f, 0.f, 0.f};
-    const int nv = owns(u) ? valid_of(u) : 0;
+    const int nv = nvq0;
     if (nv < KT) mask(sc, nv);
     if constexpr (!PV) load_sub(NS, u, fr[NS & 1]);
     float alpha = 1.f;
@@ -336,7 +362,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
           sc[kb] = mfma_32x32x16(fr[j & 1][i], qf[kk], kk == 0 ? zero16() : sc[kb]);
         }
         if (j == NS) stash((u + 2) % NBUF);
-        if (j == NS + 1 || (NQS == 1 && j == NS)) fetch(u + 3);
+        if (j == NS + 1 || (NQS == 1 && j == NS)) fetch();   // tile u+3
       }
       // reads first, then MFMAs each followed by a share of the VALU work
       if (PV || j >= NS) {
@@ -349,7 +375,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       }
       __builtin_amdgcn_sched_barrier(0);
       if (j == NS - 1) {
-        if (alpha != 1.f) {
+        if (moved) {
           // rare: the running max moved; O already holds P(u-1).V(u-1)
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb)
@@ -363,16 +389,22 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     __builtin_amdgcn_sched_barrier(0);
     __syncthreads();
     __builtin_amdgcn_sched_barrier(0);
+    nvq0 = nvq1;
+    nvq1 = nvq2;
+    nvq2 = nvq3;
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
 
   // prologue: tiles 0 and 1 in LDS, tile 2 in flight, S(0) computed
-  fetch(0);
+  fetch();
+  nvq0 = nvq3;
   stash(0);
-  fetch(1);
+  fetch();
+  nvq1 = nvq3;
   stash(1);
-  fetch(2);
+  fetch();
+  nvq2 = nvq3;
   __syncthreads();
   bf16x8 p[NS];
   f32x16 sc[2];
