@@ -23,6 +23,8 @@ GPU receives, widened exactly):
   of Eq. 5, refresh every delta steps, (t - 1) mod delta == 0): every layer
   is suffix-only, the deep layers attending over the prefix K/V that the
   request's last refresh step computed.
+* step_multi: a batch over several cached prefixes (groups of consecutive
+  requests, each group with its own cache).
 * full_forward: the un-cached forward of (p, z_t) ("no caching"), which is
   what d = 0 must equal.
 
@@ -278,6 +280,21 @@ def step(cache, x_suffix, d, layers, cfg, requests=None):
     assert 0 <= d <= L
     idx = range(x_suffix.shape[0]) if requests is None else requests
     return np.stack([step_one(cache, x_suffix[b], d, layers, cfg) for b in idx])
+
+
+def step_multi(caches, counts, x_suffix, d, layers, cfg):
+    """Step of a batch whose requests use several cached prefixes (the
+    multi-tenant setting of Sec. 6.5; each request's prefix is looked up in H,
+    Sec. 5.2): group g is counts[g] consecutive requests of x_suffix
+    [B, n_s, h] over caches[g].  Every request is step_one over its own
+    group's cache.  Returns [B, n_s, h]."""
+    assert len(caches) == len(counts) and sum(counts) == len(x_suffix)
+    out, i = [], 0
+    for cache, cnt in zip(caches, counts):
+        for _ in range(cnt):
+            out.append(step_one(cache, x_suffix[i], d, layers, cfg))
+            i += 1
+    return np.stack(out)
 
 
 def full_forward(x_prefix, x_suffix_one, layers, cfg, record=None):

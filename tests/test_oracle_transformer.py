@@ -356,3 +356,43 @@ def test_denoise_steps_schedule(setup):
     # requests stay independent across the whole sequence
     one = T.denoise_steps(cache, xsteps[:, 1:2], d, 3, layers, cfg)
     np.testing.assert_allclose(one[:, 0], base[:, 1], atol=1e-13)
+
+
+# ---------------------------------------------------------------- several prefixes
+
+def test_multi_prefix_d0_is_each_requests_full_forward():
+    """d = 0 is no caching (Sec. 3.1): with several prefixes of different
+    lengths in one batch, every request equals the un-cached forward of its own
+    (prefix, suffix), whatever the other groups hold."""
+    cfg = _cfg()
+    rng = np.random.default_rng(8)
+    layers = _weights(cfg, rng, scale_out=1 / math.sqrt(6))
+    prefixes = [rng.normal(size=(m, cfg["hidden"])) for m in (7, 3, 10)]
+    counts = [2, 1, 3]
+    xs = rng.normal(size=(sum(counts), 4, cfg["hidden"]))
+    caches = [T.populate(p, layers, cfg, cfg["n_layers"]) for p in prefixes]
+    got = T.step_multi(caches, counts, xs, 0, layers, cfg)
+    owner = [g for g, c in enumerate(counts) for _ in range(c)]
+    for b, g in enumerate(owner):
+        full = T.full_forward(prefixes[g], xs[b], layers, cfg)
+        np.testing.assert_allclose(got[b], full[len(prefixes[g]):], atol=1e-12)
+
+
+def test_multi_prefix_groups_are_independent_and_use_their_own_prefix():
+    cfg = _cfg()
+    rng = np.random.default_rng(9)
+    layers = _weights(cfg, rng, scale_out=1 / math.sqrt(6))
+    pa, pb = rng.normal(size=(6, cfg["hidden"])), rng.normal(size=(9, cfg["hidden"]))
+    ca = T.populate(pa, layers, cfg, cfg["n_layers"])
+    cb = T.populate(pb, layers, cfg, cfg["n_layers"])
+    xs = rng.normal(size=(3, 5, cfg["hidden"]))
+    for d in (1, 3):
+        both = T.step_multi([ca, cb], [1, 2], xs, d, layers, cfg)
+        np.testing.assert_allclose(both[:1], T.step(ca, xs[:1], d, layers, cfg), atol=1e-13)
+        np.testing.assert_allclose(both[1:], T.step(cb, xs[1:], d, layers, cfg), atol=1e-13)
+        # the same requests over the other prefix give other outputs
+        swapped = T.step_multi([cb, ca], [1, 2], xs, d, layers, cfg)
+        assert np.abs(swapped - both).max() > 1e-6
+        # one group of one prefix is the single-prefix step
+        np.testing.assert_allclose(T.step_multi([ca], [3], xs, d, layers, cfg),
+                                   T.step(ca, xs, d, layers, cfg), atol=1e-13)
