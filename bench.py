@@ -16,8 +16,9 @@ Prints ONE JSON line: request-denoise-steps/s of that step (value), the
 roofline of its dominant kernel (the gate/up + SwiGLU GEMM) measured live with
 HIP events inside the timed region, the fp64 CPU oracle timed on a bounded
 sample (rank 0), plus the per-depth step times, the deep-layer reuse steps of
-Eq. 5 (refresh, reuse, and their mix at refresh interval 16), and the
-shared-prefix attention throughput of the attention-only workloads.
+Eq. 5 (refresh, reuse, and their mix at refresh interval 16), a batch over
+four prefixes of different lengths, and the shared-prefix attention
+throughput of the attention-only workloads.
 """
 import argparse
 import json
@@ -221,6 +222,34 @@ def main():
         del store
         torch.cuda.empty_cache()
 
+    # ------------------------------------------------ several prefixes (Sec. 6.5)
+    # four tenants' prefixes of different lengths, four requests each, in one
+    # batch, against the same groups stepped one after another
+    mt_m = (1536, 1024, 2048, 512)
+    mt_keys = [key]
+    for i, mm in enumerate(mt_m[1:]):
+        k_i = bc.prefix_key([10 ** 6 * (i + 1) + t for t in range(mm)])
+        model.populate(k_i, synth.gaussian((mm, cfg["hidden"]), 4200 + i, device=dev), L)
+        mt_keys.append(k_i)
+    mt_counts = [B // 4] * 4
+    t_multi = timed(lambda: model.step_multi(mt_keys, mt_counts, xs, d, out=out), args.depth_steps)
+    xs_parts = [xs[i * (B // 4):(i + 1) * (B // 4)].contiguous() for i in range(4)]
+
+    def separate():
+        for k_i, x_i in zip(mt_keys, xs_parts):
+            model.step(k_i, x_i, d)
+    t_sep = timed(separate, args.depth_steps)
+    mt_flops = sum(step_flops(cfg, B // 4, mm, n_s, d) for mm in mt_m)
+    multi_prefix = {"prefixes": list(mt_m), "requests_per_prefix": B // 4, "depth": d,
+                    "batched_ms": round(t_multi, 3), "separate_ms": round(t_sep, 3),
+                    "request_steps_per_s": round(B / (t_multi / 1e3), 2),
+                    "tflops": round(mt_flops / (t_multi / 1e3) / 1e12, 1),
+                    "speedup_vs_separate": round(t_sep / t_multi, 3)}
+    for k_i in mt_keys[1:]:
+        model.invalidate(k_i)
+    del xs_parts
+    torch.cuda.empty_cache()
+
     # C4 populate: 8 layers of the same shape over an 8192-token prefix
     xp4 = synth.gaussian((8192, cfg["hidden"]), 4100, device=dev)
     key4 = bc.prefix_key(range(8192))
@@ -288,6 +317,7 @@ def main():
         "cpu_baseline": cpu,
         "per_depth": per_depth,
         "deep_reuse": deep_reuse,
+        "multi_prefix": multi_prefix,
         "kernel_ms_one_step": breakdown,
         "attention": attention,
         "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},

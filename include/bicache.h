@@ -187,6 +187,38 @@ bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int*
 bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
                           int d, float* out, void* workspace, size_t ws_bytes, void* stream);
 
+/* ----------------------------------------------- batches of several prefixes
+ *
+ * In multi-tenant serving (Sec. 6.5) the requests of one batch come with
+ * different shared prefixes: each request's prefix p is looked up in H under
+ * k = h(p) (Sec. 5.2).  A batch is given as n_groups groups: group g holds
+ * counts[g] consecutive requests of x_suffix that share the cached prefix
+ * keys[g] (its own m_g).  Every request is computed exactly as in a
+ * single-prefix step over its own prefix (requests never attend to each
+ * other); one reuse depth d applies to the whole batch. */
+
+/* Device workspace bytes that bc_step_forward_multi needs; 0 if an argument
+ * is invalid or a key is not cached. */
+size_t bc_step_multi_workspace_bytes(const bc_model* model, const uint64_t* keys, const int* counts,
+                                     int n_groups, int n_s, int d);
+
+/* One denoising step (Eq. 4 for l < d, refresh case of Eq. 5 for l >= d) of a
+ * batch over several cached prefixes.
+ *   keys, counts  host arrays of n_groups entries, 1 <= n_groups <= 4096,
+ *                 counts[g] >= 1; a key may appear in several groups
+ *   x_suffix      device bf16 [B, n_s, h], B = sum of counts; request i of
+ *                 group g is row block (counts[0] + ... + counts[g-1] + i);
+ *                 its positions are m_g..m_g+n_s-1
+ *   d             0 <= d <= L and d <= every entry's Lc
+ *   out           device fp32 [B, n_s, h], same request order
+ *   workspace     device, >= bc_step_multi_workspace_bytes(...) bytes
+ * The Q/K/V projection and the attention run once per group, every other
+ * kernel once over the whole batch.  Errors: BC_E_NOT_FOUND if any key is not
+ * cached, BC_E_INVALID for bad sizes, pointers or d. */
+bc_status bc_step_forward_multi(bc_model* model, const uint64_t* keys, const int* counts,
+                                int n_groups, const void* x_suffix, int n_s, int d, float* out,
+                                void* workspace, size_t ws_bytes, void* stream);
+
 /* ------------------------------------------------- deep-layer reuse (Eq. 5)
  *
  * Within one request the deep layers (l >= d) need not recompute the prefix
@@ -250,7 +282,9 @@ bc_status bc_deep_store_reset(bc_model* model, const void* deep_store);
  *               (a reuse step needs no more than
  *               bc_step_workspace_bytes(model, m, B, n_s, L))
  * Other arguments and errors as bc_step_forward; a refresh of a batch is for
- * all its requests at once (per-request schedules need separate batches). */
+ * all its requests at once (per-request schedules need separate batches), and
+ * the batch shares one prefix (a multi-prefix batch keeps a store per prefix
+ * group by stepping each group as its own batch). */
 bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suffix, int B,
                                int n_s, int d, int mode, void* deep_store, size_t store_bytes,
                                float* out, void* workspace, size_t ws_bytes, void* stream);

@@ -60,6 +60,11 @@ _SIGS = {
     "bc_shared_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
     "bc_request_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
     "bc_is_refresh_step": (C.c_int, [C.c_int, C.c_int]),
+    "bc_step_multi_workspace_bytes": (C.c_size_t, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_int),
+                                                   C.c_int, C.c_int, C.c_int]),
+    "bc_step_forward_multi": (C.c_int, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_int), C.c_int,
+                                        C.c_void_p, C.c_int, C.c_int, C.c_void_p, C.c_void_p, C.c_size_t,
+                                        C.c_void_p]),
     "bc_deep_store_reset": (C.c_int, [C.c_void_p, C.c_void_p]),
     "bc_deep_store_bytes": (C.c_size_t, [C.c_void_p, C.c_int, C.c_int, C.c_int, C.c_int]),
     "bc_deep_store_offset": (C.c_size_t, [C.c_void_p] + [C.c_int] * 10),
@@ -286,6 +291,30 @@ class Model:
         rh = C.c_int()
         _check(lib().bc_step_plan(self._h, m, B, n_s, d, rows, pos, kv, C.byref(rh)))
         return list(rows), list(pos), list(kv), rh.value
+
+    def step_multi(self, keys, counts, x_suffix, d, out=None):
+        """Step of a batch over several cached prefixes: group g is counts[g]
+        consecutive requests of x_suffix [B, n_s, h] (bf16, device) sharing the
+        prefix keys[g].  Returns the fp32 suffix rows [B, n_s, h]."""
+        B, n_s, h = x_suffix.shape
+        G = len(keys)
+        if len(counts) != G or sum(counts) != B:
+            raise ValueError(f"counts {list(counts)} do not cover the batch of {B}")
+        karr = (C.c_uint64 * G)(*[int(k) for k in keys])
+        carr = (C.c_int * G)(*[int(c) for c in counts])
+        wsb = int(lib().bc_step_multi_workspace_bytes(self._h, karr, carr, G, n_s, d))
+        if wsb == 0:
+            missing = [k for k in keys if self.lookup(k) is None]
+            if missing:
+                raise BiCacheError(-2, f"keys {[hex(k) for k in missing]} are not cached")
+            raise BiCacheError(-1, f"invalid multi-prefix step counts={list(counts)} n_s={n_s} d={d}")
+        ws = self._workspace(wsb, x_suffix.device)
+        if out is None:
+            out = torch.empty((B, n_s, h), dtype=torch.float32, device=x_suffix.device)
+        _check(lib().bc_step_forward_multi(self._h, karr, carr, G, _dev(x_suffix, torch.bfloat16, "x_suffix"),
+                                           n_s, d, _dev(out, torch.float32, "out"),
+                                           C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
+        return out
 
     def deep_store_bytes(self, m, B, n_s, d):
         return int(lib().bc_deep_store_bytes(self._h, m, B, n_s, d))

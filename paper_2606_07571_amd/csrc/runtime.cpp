@@ -73,6 +73,7 @@ bc_status ok() {
 }
 
 constexpr size_t kAlign = 256;
+constexpr int kMaxGroups = 4096;  // prefix groups in one batch
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
 // Sub-buffer plan of a workspace.  All offsets are 256-byte aligned.
@@ -197,15 +198,18 @@ hipError_t prof_mark(bc_model* mdl, int kind, hipStream_t s, size_t* idx) {
     if (i0_ != SIZE_MAX) mdl->prof.recs.push_back({kind, i0_, i1_});             \
   } while (0)
 
-// One transformer layer over `rows` = n_req * n_seq token rows held in the fp32
-// residual R.  Row r is token t = r % n_seq of request r / n_seq at RoPE
-// position pos0 + t.  The layer's own K/V are written to k_dst/v_dst
-// (element (req, head, t, dim) at req*kv_sb + head*kv_sh + t*dh + dim).
-// Attention of every request runs over [kp/vp (m_pre prefix rows, may be 0) ;
-// its own n_seq keys]; the prefix is shared by all requests when kp_sb == 0,
-// else request r's starts at kp + r*kp_sb (head stride kp_sh, 0 = m_pre*dh).
-struct LayerCall {
-  float* R;
+// One transformer layer over the token rows held in the fp32 residual R.  The
+// rows form segments; segment i covers rows [row0, row0 + n_req*n_seq), row
+// row0 + r being token t = r % n_seq of its request r / n_seq at RoPE position
+// pos0 + t.  A segment's own K/V are written to k_dst/v_dst (element (req,
+// head, t, dim) at req*kv_sb + head*kv_sh + t*dh + dim) and each of its
+// requests attends over [kp/vp (m_pre prefix rows, may be 0) ; its own n_seq
+// keys]; the prefix is shared by the segment's requests when kp_sb == 0, else
+// request r's starts at kp + r*kp_sb (head stride kp_sh, 0 = m_pre*dh).
+// Normalisation and the O / FFN GEMMs run once over all rows (rows are
+// independent there); the Q/K/V projection and the attention run per segment.
+struct Seg {
+  long row0;
   int n_req, n_seq, pos0;
   const void* kp;
   const void* vp;
@@ -216,53 +220,65 @@ struct LayerCall {
   long kp_sb = 0, kp_sh = 0;
 };
 
+struct LayerCall {
+  float* R;
+  long rows;
+  const Seg* segs;
+  int n_segs;
+};
+
 bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const Plan& p,
                     hipStream_t s) {
   const bc_model_config& c = mdl->cfg;
   const bc_layer_weights& w = mdl->layers[l];
   const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
-  const int rows = lc.n_req * lc.n_seq;
+  const int rows = (int)lc.rows;
   const int hd = Hq * dh;
-  void* xn = ws + p.xn;
-  void* q = ws + p.q;
-  void* ao = ws + p.ao;
+  uint16_t* xn = (uint16_t*)(ws + p.xn);  // bf16 bits
+  uint16_t* q = (uint16_t*)(ws + p.q);
+  uint16_t* ao = (uint16_t*)(ws + p.ao);
   void* act = ws + p.act;
   const float* cos_t = (const float*)(ws + p.cos);
   const float* sin_t = (const float*)(ws + p.sin);
 
   BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.attn_norm, xn, rows, h, c.rms_eps, s));
-  bc::QkvOut qo{q, lc.k_dst, lc.v_dst, (long)Hq * lc.n_seq * dh, (long)lc.n_seq * dh,
-                lc.kv_sb, lc.kv_sh, lc.kv_sb, lc.kv_sh};
-  BC_LAUNCH(mdl, BC_K_QKV, s,
-            bc::gemm_qkv_rope(xn, h, w.w_qkv, h, rows, h, Hq, Hkv, dh, lc.n_seq, lc.pos0, cos_t,
-                              sin_t, qo, s));
-  bc::AttnArgs a{};
-  a.q = q;
-  a.q_sb = (long)Hq * lc.n_seq * dh;
-  a.q_sh = (long)lc.n_seq * dh;
-  a.q_sr = dh;
-  a.kp = lc.kp;
-  a.vp = lc.vp;
-  a.p_sb = lc.kp_sb;
-  a.p_sh = lc.kp_sh ? lc.kp_sh : (long)lc.m_pre * dh;
-  a.ks = lc.k_dst;
-  a.vs = lc.v_dst;
-  a.s_sb = lc.kv_sb;
-  a.s_sh = lc.kv_sh;
-  a.s_sr = dh;
-  a.out = ao;  // token-major [req, t, head, dim]: the O projection's A operand
-  a.o_sb = (long)lc.n_seq * hd;
-  a.o_sh = dh;
-  a.o_sr = hd;
-  a.B = lc.n_req;
-  a.Hq = Hq;
-  a.Hkv = Hkv;
-  a.m = lc.m_pre;
-  a.n_s = lc.n_seq;
-  a.dh = dh;
-  a.scale = 1.f / sqrtf((float)dh);
-  a.out_f32 = 0;
-  BC_LAUNCH(mdl, lc.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
+  for (int i = 0; i < lc.n_segs; ++i) {
+    const Seg& g = lc.segs[i];
+    const int seg_rows = g.n_req * g.n_seq;
+    uint16_t* qg = q + g.row0 * hd;
+    bc::QkvOut qo{qg, g.k_dst, g.v_dst, (long)Hq * g.n_seq * dh, (long)g.n_seq * dh,
+                  g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh};
+    BC_LAUNCH(mdl, BC_K_QKV, s,
+              bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, seg_rows, h, Hq, Hkv, dh, g.n_seq,
+                                g.pos0, cos_t, sin_t, qo, s));
+    bc::AttnArgs a{};
+    a.q = qg;
+    a.q_sb = (long)Hq * g.n_seq * dh;
+    a.q_sh = (long)g.n_seq * dh;
+    a.q_sr = dh;
+    a.kp = g.kp;
+    a.vp = g.vp;
+    a.p_sb = g.kp_sb;
+    a.p_sh = g.kp_sh ? g.kp_sh : (long)g.m_pre * dh;
+    a.ks = g.k_dst;
+    a.vs = g.v_dst;
+    a.s_sb = g.kv_sb;
+    a.s_sh = g.kv_sh;
+    a.s_sr = dh;
+    a.out = ao + g.row0 * hd;  // token-major [req, t, head, dim]: the O projection's A operand
+    a.o_sb = (long)g.n_seq * hd;
+    a.o_sh = dh;
+    a.o_sr = hd;
+    a.B = g.n_req;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.m = g.m_pre;
+    a.n_s = g.n_seq;
+    a.dh = dh;
+    a.scale = 1.f / sqrtf((float)dh);
+    a.out_f32 = 0;
+    BC_LAUNCH(mdl, g.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
+  }
   BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, lc.R, h, s));
   BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.ffn_norm, xn, rows, h, c.rms_eps, s));
   BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
@@ -294,33 +310,61 @@ bool step_shape_ok(const bc_model_config& c, int m, int B, int n_s, int d, std::
 }
 
 
-// Both kinds of step.  mode BC_DEEP_REFRESH: layers l < d suffix-only over
-// KV$_l, layers l >= d recompute the prefix from H$_d (their K/V of every row
-// go to `store` when it is non-null, else to the workspace).  BC_DEEP_REUSE:
-// every layer suffix-only, deep layers over the request's prefix rows in
-// `store`.
-bc_status step_impl(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s, int d,
-                    int mode, void* store, size_t store_bytes, float* out, void* workspace,
-                    size_t ws_bytes, void* stream) {
-  if (!model || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+// A group of a batch: `count` consecutive requests over the cached prefix
+// `key` (one group unless the batch spans several prefixes).
+struct Group {
+  uint64_t key;
+  int count;
+};
+
+// The step, for every kind: mode BC_DEEP_REFRESH: layers l < d suffix-only
+// over KV$_l, layers l >= d recompute the prefix from H$_d (their K/V of every
+// row go to `store` when it is non-null, else to the workspace).
+// BC_DEEP_REUSE: every layer suffix-only, deep layers over the request's
+// prefix rows in `store`.  The deep store is for single-prefix batches only.
+// Work layout with several groups: the shallow residual is `out` [B][n_s][h]
+// (group g's requests at rows first_g*n_s...); the deep residual, Q/K/V and
+// attention output hold the groups one after another, group g's requests
+// with N_g = m_g + n_s rows each.
+bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const void* x_suffix,
+                    int n_s, int d, int mode, void* store, size_t store_bytes, float* out,
+                    void* workspace, size_t ws_bytes, void* stream) {
+  if (!model || !groups || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
   if (mode != BC_DEEP_REFRESH && mode != BC_DEEP_REUSE) return fail(BC_E_INVALID, "unknown deep mode %d", mode);
+  if (n_groups < 1 || n_groups > kMaxGroups)
+    return fail(BC_E_INVALID, "n_groups=%d outside [1, %d]", n_groups, kMaxGroups);
   const bc_model_config& c = model->cfg;
   const int L = c.n_layers;
-  const bc::CacheEntry* ent = model->table.find(key);
-  if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
-  const int m = ent->m;
+  std::vector<const bc::CacheEntry*> ents(n_groups);
+  long B = 0, full_rows = 0;
+  int max_N = 0;
   std::string why;
-  if (!step_shape_ok(c, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
-  if (d > ent->n_layers)
-    return fail(BC_E_INVALID, "reuse depth d=%d exceeds the %d cached layers of this prefix", d, ent->n_layers);
-  const long N = (long)m + n_s;
-  const bool full = mode == BC_DEEP_REFRESH && d < L;  // deep layers run over all N rows
-  const long rows_max = (long)B * (full ? N : n_s);
-  const Plan p = make_plan(c, rows_max, N, true, full ? (long)B * N : 0);
+  for (int g = 0; g < n_groups; ++g) {
+    ents[g] = model->table.find(groups[g].key);
+    if (!ents[g]) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)groups[g].key);
+    const int m = ents[g]->m;
+    if (groups[g].count < 1) return fail(BC_E_INVALID, "group %d has count %d < 1", g, groups[g].count);
+    if (!step_shape_ok(c, m, groups[g].count, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+    if (d > ents[g]->n_layers)
+      return fail(BC_E_INVALID, "reuse depth d=%d exceeds the %d cached layers of prefix %016llx", d,
+                  ents[g]->n_layers, (unsigned long long)groups[g].key);
+    B += groups[g].count;
+    full_rows += (long)groups[g].count * (m + n_s);
+    if (m + n_s > max_N) max_N = m + n_s;
+  }
+  if (B > INT_MAX / 2 || full_rows > INT_MAX / 2 || full_rows * (long)c.hidden > (1L << 40))
+    return fail(BC_E_INVALID, "step too large (B=%ld, %ld full rows)", B, full_rows);
+  const bool full = mode == BC_DEEP_REFRESH && d < L;  // deep layers run over all rows
+  const long rows_max = full ? full_rows : B * n_s;
+  const Plan p = make_plan(c, rows_max, max_N, true, full ? full_rows : 0);
   if (ws_bytes < p.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, p.total);
   if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
-  const DeepLayout dl = deep_layout(c, m, B, n_s, d);
   const bool use_store = d < L && (mode == BC_DEEP_REUSE || store);
+  if (use_store && n_groups != 1)
+    return fail(BC_E_INVALID, "deep-layer reuse (deep store) needs a single-prefix batch");
+  const int m0 = ents[0]->m;
+  const uint64_t key0 = groups[0].key;
+  const DeepLayout dl = deep_layout(c, m0, (int)B, n_s, d);
   if (use_store) {
     if (!store) return fail(BC_E_INVALID, "a reuse step at d=%d < L needs the deep store", d);
     if (store_bytes < dl.total) return fail(BC_E_INVALID, "deep store %zu < required %zu", store_bytes, dl.total);
@@ -331,57 +375,105 @@ bc_status step_impl(bc_model* model, uint64_t key, const void* x_suffix, int B, 
     if (it == model->deep_tags.end())
       return fail(BC_E_STATE, "no refresh step has written this deep store");
     const DeepTag& tg = it->second;
-    if (tg.key != key || tg.m != m || tg.B != B || tg.n_s != n_s || tg.d != d)
+    if (tg.key != key0 || tg.m != m0 || tg.B != B || tg.n_s != n_s || tg.d != d)
       return fail(BC_E_STATE,
-                  "deep store was refreshed for key %016llx m=%d B=%d n_s=%d d=%d, not key %016llx m=%d B=%d n_s=%d d=%d",
-                  (unsigned long long)tg.key, tg.m, tg.B, tg.n_s, tg.d, (unsigned long long)key, m, B, n_s, d);
+                  "deep store was refreshed for key %016llx m=%d B=%d n_s=%d d=%d, not key %016llx m=%d B=%ld n_s=%d d=%d",
+                  (unsigned long long)tg.key, tg.m, tg.B, tg.n_s, tg.d, (unsigned long long)key0, m0, B, n_s, d);
   }
 
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
   char* st_mem = (char*)store;
-  const char* cm = (const char*)ent->mem;
-  const EntryLayout e = entry_layout(c, m, ent->n_layers);
-  const int dh = c.head_dim, Hkv = c.n_kv_heads;
+  const int dh = c.head_dim, Hkv = c.n_kv_heads, h = c.hidden;
+  const long kvd = (long)Hkv * dh;
   auto deep_k = [&](int l) { return st_mem + (size_t)(2 * (l - d)) * dl.part; };
   auto deep_v = [&](int l) { return st_mem + (size_t)(2 * (l - d) + 1) * dl.part; };
+  std::vector<Seg> segs(n_groups);
 
-  BC_LAUNCH(model, BC_K_OTHER, s, bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), (int)N, dh, c.rope_theta, s));
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::rope_table((float*)(ws + p.cos), (float*)(ws + p.sin), max_N, dh, c.rope_theta, s));
   // suffix-only residual, kept in `out`
-  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_suffix, out, (long)B * n_s * c.hidden, s));
+  BC_LAUNCH(model, BC_K_OTHER, s, bc::bf16_to_f32(x_suffix, out, B * n_s * h, s));
   const int n_suffix_layers = full ? d : L;
   for (int l = 0; l < n_suffix_layers; ++l) {
-    LayerCall lc{out, B, n_s, m, nullptr, nullptr, m,
-                 ws + p.k, ws + p.v, (long)Hkv * n_s * dh, (long)n_s * dh};
-    if (l < d) {  // Eq. 4: the shared KV$_l
-      lc.kp = cm + (size_t)(2 * l) * e.kv_layer;
-      lc.vp = cm + (size_t)(2 * l + 1) * e.kv_layer;
-    } else {      // second case of Eq. 5: this request's prefix K/V of the last refresh
-      lc.kp = deep_k(l);
-      lc.vp = deep_v(l);
-      lc.kp_sb = dl.sb;
-      lc.kp_sh = dl.sh;
+    long row0 = 0;
+    for (int g = 0; g < n_groups; ++g) {
+      const int m = ents[g]->m, cnt = groups[g].count;
+      Seg& sg = segs[g];
+      sg = Seg{row0, cnt, n_s, m, nullptr, nullptr, m,
+               ws + p.k + row0 * kvd * 2, ws + p.v + row0 * kvd * 2, kvd * n_s, (long)n_s * dh};
+      if (l < d) {  // Eq. 4: the shared KV$_l of the group's prefix
+        const EntryLayout e = entry_layout(c, m, ents[g]->n_layers);
+        const char* cm = (const char*)ents[g]->mem;
+        sg.kp = cm + (size_t)(2 * l) * e.kv_layer;
+        sg.vp = cm + (size_t)(2 * l + 1) * e.kv_layer;
+      } else {      // second case of Eq. 5: this request's prefix K/V of the last refresh
+        sg.kp = deep_k(l);
+        sg.vp = deep_v(l);
+        sg.kp_sb = dl.sb;
+        sg.kp_sh = dl.sh;
+      }
+      row0 += (long)cnt * n_s;
     }
+    LayerCall lc{out, B * n_s, segs.data(), n_groups};
     bc_status st = run_layer(model, l, lc, ws, p, s);
     if (st != BC_OK) return st;
   }
   if (full) {
     float* R = (float*)(ws + p.R);
-    const float* hd = (const float*)(cm + e.h_off + (size_t)d * e.h_layer);
-    BC_LAUNCH(model, BC_K_OTHER, s, bc::build_full_residual(hd, out, R, B, m, n_s, c.hidden, s));
+    long row0 = 0, first = 0;
+    for (int g = 0; g < n_groups; ++g) {
+      const int m = ents[g]->m, cnt = groups[g].count;
+      const EntryLayout e = entry_layout(c, m, ents[g]->n_layers);
+      const float* hdp = (const float*)((const char*)ents[g]->mem + e.h_off + (size_t)d * e.h_layer);
+      BC_LAUNCH(model, BC_K_OTHER, s,
+                bc::build_full_residual(hdp, out + first * n_s * h, R + row0 * h, cnt, m, n_s, h, s));
+      row0 += (long)cnt * (m + n_s);
+      first += cnt;
+    }
     for (int l = d; l < L; ++l) {
-      void* kd = use_store ? (void*)deep_k(l) : (void*)(ws + p.k);
-      void* vd = use_store ? (void*)deep_v(l) : (void*)(ws + p.v);
-      LayerCall lc{R, B, (int)N, 0, nullptr, nullptr, 0, kd, vd, dl.sb, dl.sh};
+      row0 = 0;
+      for (int g = 0; g < n_groups; ++g) {
+        const int N = ents[g]->m + n_s, cnt = groups[g].count;
+        void* kd = use_store ? (void*)deep_k(l) : (void*)(ws + p.k + row0 * kvd * 2);
+        void* vd = use_store ? (void*)deep_v(l) : (void*)(ws + p.v + row0 * kvd * 2);
+        segs[g] = Seg{row0, cnt, N, 0, nullptr, nullptr, 0, kd, vd, kvd * N, (long)N * dh};
+        row0 += (long)cnt * N;
+      }
+      LayerCall lc{R, full_rows, segs.data(), n_groups};
       bc_status st = run_layer(model, l, lc, ws, p, s);
       if (st != BC_OK) return st;
     }
-    BC_LAUNCH(model, BC_K_OTHER, s, bc::gather_suffix(R, out, B, m, n_s, c.hidden, s));
-    if (use_store) model->deep_tags[(uintptr_t)store] = DeepTag{key, m, B, n_s, d};
+    row0 = 0;
+    first = 0;
+    for (int g = 0; g < n_groups; ++g) {
+      const int m = ents[g]->m, cnt = groups[g].count;
+      BC_LAUNCH(model, BC_K_OTHER, s,
+                bc::gather_suffix(R + row0 * h, out + first * n_s * h, cnt, m, n_s, h, s));
+      row0 += (long)cnt * (m + n_s);
+      first += cnt;
+    }
+    if (use_store) model->deep_tags[(uintptr_t)store] = DeepTag{key0, m0, (int)B, n_s, d};
   }
   return ok();
 }
 
+// Sizes of a step over groups, for the workspace functions (0 when invalid).
+size_t step_workspace(const bc_model* model, const int* ms, const int* counts, int n_groups,
+                      int n_s, int d) {
+  const bc_model_config& c = model->cfg;
+  long B = 0, full_rows = 0;
+  int max_N = 0;
+  std::string why;
+  for (int g = 0; g < n_groups; ++g) {
+    if (!step_shape_ok(c, ms[g], counts[g], n_s, d, &why)) return 0;
+    B += counts[g];
+    full_rows += (long)counts[g] * (ms[g] + n_s);
+    if (ms[g] + n_s > max_N) max_N = ms[g] + n_s;
+  }
+  if (B > INT_MAX / 2 || full_rows > INT_MAX / 2) return 0;
+  const bool full = d < c.n_layers;
+  return make_plan(c, full ? full_rows : B * n_s, max_N, true, full ? full_rows : 0).total;
+}
 
 bc_status prefix_attention(const void* q, const void* k_pre, const void* v_pre, long pre_sb,
                            const void* k_suf, const void* v_suf, float* out, int B, int Hq,
@@ -517,7 +609,8 @@ bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix
     if (l >= Lc) break;
     char* k_dst = cm + (size_t)(2 * l) * e.kv_layer;
     char* v_dst = cm + (size_t)(2 * l + 1) * e.kv_layer;
-    LayerCall lc{R, 1, m, 0, nullptr, nullptr, 0, k_dst, v_dst, 0, (long)m * c.head_dim};
+    const Seg sg{0, 1, m, 0, nullptr, nullptr, 0, k_dst, v_dst, 0, (long)m * c.head_dim};
+    LayerCall lc{R, m, &sg, 1};
     bc_status st = run_layer(model, l, lc, ws, p, s);
     if (st != BC_OK) return st;
   }
@@ -573,12 +666,19 @@ uint64_t bc_prefix_key(const int32_t* token_ids, size_t n) {
 
 size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int d) {
   if (!model) return 0;
-  std::string why;
-  if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return 0;
-  const int L = model->cfg.n_layers;
-  const long N = (long)m + n_s;
-  const long rows = (long)B * (d < L ? N : n_s);
-  return make_plan(model->cfg, rows, N, true, d < L ? (long)B * N : 0).total;
+  return step_workspace(model, &m, &B, 1, n_s, d);
+}
+
+size_t bc_step_multi_workspace_bytes(const bc_model* model, const uint64_t* keys, const int* counts,
+                                     int n_groups, int n_s, int d) {
+  if (!model || !keys || !counts || n_groups < 1 || n_groups > kMaxGroups) return 0;
+  std::vector<int> ms(n_groups);
+  for (int g = 0; g < n_groups; ++g) {
+    const bc::CacheEntry* e = model->table.find(keys[g]);
+    if (!e) return 0;
+    ms[g] = e->m;
+  }
+  return step_workspace(model, ms.data(), counts, n_groups, n_s, d);
 }
 
 bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int* rows,
@@ -600,7 +700,8 @@ bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int*
 
 bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
                           int d, float* out, void* workspace, size_t ws_bytes, void* stream) {
-  return step_impl(model, key, x_suffix, B, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out, workspace,
+  const Group g{key, B};
+  return step_impl(model, &g, 1, x_suffix, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out, workspace,
                    ws_bytes, stream);
 }
 
@@ -640,8 +741,21 @@ int bc_is_refresh_step(int t, int delta) {
 bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suffix, int B,
                                int n_s, int d, int mode, void* deep_store, size_t store_bytes,
                                float* out, void* workspace, size_t ws_bytes, void* stream) {
-  return step_impl(model, key, x_suffix, B, n_s, d, mode, deep_store, store_bytes, out, workspace,
+  const Group g{key, B};
+  return step_impl(model, &g, 1, x_suffix, n_s, d, mode, deep_store, store_bytes, out, workspace,
                    ws_bytes, stream);
+}
+
+bc_status bc_step_forward_multi(bc_model* model, const uint64_t* keys, const int* counts,
+                                int n_groups, const void* x_suffix, int n_s, int d, float* out,
+                                void* workspace, size_t ws_bytes, void* stream) {
+  if (!keys || !counts) return fail(BC_E_INVALID, "null argument");
+  if (n_groups < 1 || n_groups > kMaxGroups)
+    return fail(BC_E_INVALID, "n_groups=%d outside [1, %d]", n_groups, kMaxGroups);
+  std::vector<Group> gs(n_groups);
+  for (int g = 0; g < n_groups; ++g) gs[g] = Group{keys[g], counts[g]};
+  return step_impl(model, gs.data(), n_groups, x_suffix, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out,
+                   workspace, ws_bytes, stream);
 }
 
 bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) {
