@@ -16,9 +16,10 @@ Prints ONE JSON line: request-denoise-steps/s of that step (value), the
 roofline of its dominant kernel (the gate/up + SwiGLU GEMM) measured live with
 HIP events inside the timed region, the fp64 CPU oracle timed on a bounded
 sample (rank 0), plus the per-depth step times, the deep-layer reuse steps of
-Eq. 5 (refresh, reuse, and their mix at refresh interval 16), a batch over
-four prefixes of different lengths, and the shared-prefix attention
-throughput of the attention-only workloads.
+Eq. 5 (refresh, reuse, and their mix at refresh interval 16), the profiling
+pass of Eq. 3 (KV similarity of every request and layer), a batch over four
+prefixes of different lengths, and the shared-prefix attention throughput of
+the attention-only workloads.
 """
 import argparse
 import json
@@ -222,6 +223,27 @@ def main():
         del store
         torch.cuda.empty_cache()
 
+    # ------------------------------------------------ profiling (Eq. 3, Sec. 5.1)
+    # sim_{l,1} of the 16 requests at every layer: the un-cached step storing
+    # every layer's K/V, then the HBM-bound similarity reduction per layer
+    sims = model.profile_similarity(key, xs)
+    torch.cuda.synchronize()
+    t_prof = timed(lambda: model.profile_similarity(key, xs, sims=sims), args.depth_steps)
+    model.profile_begin(["kv_similarity"])
+    model.profile_similarity(key, xs, sims=sims)
+    sim_ms, sim_n = model.profile_end()["kv_similarity"]
+    Hkv, dh = cfg["n_kv_heads"], cfg["head_dim"]
+    kv_layer_bytes = 2 * Hkv * m * dh * 2
+    sim_bytes = L * (kv_layer_bytes + B * kv_layer_bytes)   # KV$ once, each request's KV^ref once
+    profiling = {"requests": B, "layers": L, "profile_ms": round(t_prof, 3),
+                 "similarity_ms": round(sim_ms, 4), "similarity_launch_pairs": sim_n,
+                 "similarity_bytes": sim_bytes,
+                 "similarity_gbs": round(sim_bytes / (sim_ms / 1e3) / 1e9, 1),
+                 "similarity_frac_of_hbm": round(sim_bytes / (sim_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
+                 "sim_layer_mean_min": [round(float(x), 6) for x in (sims.mean().item(), sims.min().item())]}
+    del sims
+    torch.cuda.empty_cache()
+
     # ------------------------------------------------ several prefixes (Sec. 6.5)
     # four tenants' prefixes of different lengths, four requests each, in one
     # batch, against the same groups stepped one after another
@@ -318,6 +340,7 @@ def main():
         "per_depth": per_depth,
         "deep_reuse": deep_reuse,
         "multi_prefix": multi_prefix,
+        "profiling": profiling,
         "kernel_ms_one_step": breakdown,
         "attention": attention,
         "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},

@@ -289,6 +289,61 @@ bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suff
                                int n_s, int d, int mode, void* deep_store, size_t store_bytes,
                                float* out, void* workspace, size_t ws_bytes, void* stream);
 
+/* ---------------------------------------------- shared-prefix profiling
+ *
+ * Offline profiling (Sec. 5.1) measures, for a request with prefix p and
+ * suffix z, the KV similarity of Eq. 3 at the first step for every layer:
+ *   sim_l = cos(flatten(KV$_l), flatten(KV^ref_{l,1}))
+ * where KV$_l are the cached prefix-only KVs and KV^ref_{l,1} the prefix
+ * rows' KVs of the un-cached forward of (p, z); K and V of every head and
+ * position form one vector.  The shallow depth of the request is the largest
+ * b with sim_l >= tau for every 1-based layer l <= b (Sec. 4.2), and the
+ * lookup table T maps the shared-prefix ratio r = m / (m + n_s) to the mean b
+ * of the profiled requests at that r. */
+
+/* Device workspace bytes of bc_profile_similarity. */
+size_t bc_profile_workspace_bytes(const bc_model* model, int m, int B, int n_s);
+
+/* sim_l of B requests over the cached prefix `key`, which must cache all L
+ * layers (n_layers_to_cache = L at populate).
+ *   x_suffix  device bf16 [B, n_s, h]: the requests' non-shared rows at the
+ *             first step (positions m..m+n_s-1)
+ *   sims      device fp64 [B, L]: sims[b*L + l] = sim of 0-based layer l
+ *   workspace device, >= bc_profile_workspace_bytes(model, m, B, n_s) bytes
+ * Runs the un-cached step (d = 0) storing every layer's K/V, then one
+ * HBM-bound reduction per layer (fp32 lane sums, fp64 across lanes and
+ * workgroups, fixed order: results repeat bit for bit).  Errors as
+ * bc_step_forward; BC_E_INVALID if the entry caches fewer than L layers. */
+bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
+                                double* sims, void* workspace, size_t ws_bytes, void* stream);
+
+/* Device workspace bytes of bc_cosine_similarity (0 if n is invalid). */
+size_t bc_cosine_workspace_bytes(long n);
+
+/* *out = cos(a, b) of two bf16 device vectors of n elements (n a positive
+ * multiple of 8, 16-byte aligned), into device fp64 memory, with the same
+ * reduction as bc_profile_similarity.  A zero vector gives NaN. */
+bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out, void* workspace,
+                               size_t ws_bytes, void* stream);
+
+/* The shallow depth b of Sec. 4.2: the number of leading entries of
+ * sims[0..n_layers) that are >= tau (0..n_layers); -1 for bad arguments.
+ * Host only. */
+int bc_shallow_depth(const double* sims, int n_layers, double tau);
+
+/* Table T (Sec. 5.1) over ratio buckets r = k / n_buckets, k = 1..n_buckets:
+ * request i (ratio ratios[i], which must be a bucket value, and profiled
+ * depth depths[i] >= 0) falls into bucket k; table[k] = floor(mean depth of
+ * bucket k), or -1 for a bucket without requests; table[0] = -1.  table has
+ * n_buckets + 1 entries.  Host only. */
+bc_status bc_build_depth_table(const double* ratios, const int* depths, int n, int n_buckets,
+                               int* table);
+
+/* d for a request of shared-prefix ratio r: table[k] of the largest bucket
+ * k <= r * n_buckets that has data (rounding down is the safe side, as b
+ * grows with r); 0 if none; -1 for bad arguments.  Host only. */
+int bc_depth_lookup(const int* table, int n_buckets, double r);
+
 /* ------------------------------------------------------------ profiling */
 
 /* Kernel classes of the step and of populate, for bc_profile_* below. */
@@ -302,7 +357,8 @@ enum {
   BC_K_GATE_UP = 5,     /* gate/up projection + SwiGLU */
   BC_K_DOWN = 6,        /* down projection + residual add */
   BC_K_OTHER = 7,       /* RoPE table, input widening, transition, suffix gather */
-  BC_K_COUNT = 8
+  BC_K_KVSIM = 8,       /* KV-similarity reduction of bc_profile_similarity */
+  BC_K_COUNT = 9
 };
 
 /* Starts timing, with HIP events recorded on the launch stream around every

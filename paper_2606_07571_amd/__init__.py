@@ -4,5 +4,6 @@ The computation lives in libbicache.so (hand-written HIP kernels behind a C
 ABI, declared in include/bicache.h); this package is a thin ctypes binding
 over it plus the seeded synthetic-input generators used by tests and bench.
 """
-from ._lib import (BiCacheError, LIB_PATH, Model, is_refresh_step, lib, prefix_key,  # noqa: F401
-                   request_prefix_attention, shared_prefix_attention)
+from ._lib import (BiCacheError, LIB_PATH, Model, build_depth_table, cosine_similarity,  # noqa: F401
+                   depth_lookup, is_refresh_step, lib, prefix_key, request_prefix_attention,
+                   shallow_depth, shared_prefix_attention)

@@ -60,6 +60,16 @@ _SIGS = {
     "bc_shared_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
     "bc_request_prefix_attention": (C.c_int, [C.c_void_p] * 6 + [C.c_int] * 6 + [C.c_float, C.c_void_p]),
     "bc_is_refresh_step": (C.c_int, [C.c_int, C.c_int]),
+    "bc_profile_workspace_bytes": (C.c_size_t, [C.c_void_p, C.c_int, C.c_int, C.c_int]),
+    "bc_profile_similarity": (C.c_int, [C.c_void_p, C.c_uint64, C.c_void_p, C.c_int, C.c_int, C.c_void_p,
+                                        C.c_void_p, C.c_size_t, C.c_void_p]),
+    "bc_cosine_workspace_bytes": (C.c_size_t, [C.c_long]),
+    "bc_cosine_similarity": (C.c_int, [C.c_void_p, C.c_void_p, C.c_long, C.c_void_p, C.c_void_p,
+                                       C.c_size_t, C.c_void_p]),
+    "bc_shallow_depth": (C.c_int, [C.POINTER(C.c_double), C.c_int, C.c_double]),
+    "bc_build_depth_table": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int), C.c_int, C.c_int,
+                                       C.POINTER(C.c_int)]),
+    "bc_depth_lookup": (C.c_int, [C.POINTER(C.c_int), C.c_int, C.c_double]),
     "bc_step_multi_workspace_bytes": (C.c_size_t, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_int),
                                                    C.c_int, C.c_int, C.c_int]),
     "bc_step_forward_multi": (C.c_int, [C.c_void_p, C.POINTER(C.c_uint64), C.POINTER(C.c_int), C.c_int,
@@ -77,7 +87,7 @@ _SIGS = {
 
 # kernel classes of bc_profile_* (include/bicache.h)
 KERNEL_CLASSES = ("rmsnorm", "qkv_rope", "attn_shared", "attn_full", "o_proj", "gate_up_swiglu",
-                  "down", "other")
+                  "down", "other", "kv_similarity")
 
 _lib = None
 
@@ -168,6 +178,50 @@ def is_refresh_step(t, delta):
     if r < 0:
         raise BiCacheError(-1, f"invalid step t={t} or refresh interval delta={delta}")
     return bool(r)
+
+
+def cosine_similarity(a, b):
+    """cos(a, b) of two bf16 device vectors (numel a multiple of 8), as a
+    0-d fp64 device tensor."""
+    n = a.numel()
+    if b.numel() != n:
+        raise ValueError("operands differ in size")
+    wsb = int(lib().bc_cosine_workspace_bytes(n))
+    if wsb == 0:
+        raise BiCacheError(-1, f"n={n} must be a positive multiple of 8")
+    ws = torch.empty(wsb, dtype=torch.uint8, device=a.device)
+    out = torch.empty((), dtype=torch.float64, device=a.device)
+    _check(lib().bc_cosine_similarity(_dev(a, torch.bfloat16, "a"), _dev(b, torch.bfloat16, "b"), n,
+                                      C.c_void_p(out.data_ptr()), C.c_void_p(ws.data_ptr()), wsb, _stream()))
+    return out
+
+
+def shallow_depth(sims, tau):
+    """Sec. 4.2 rule on a host sequence of per-layer similarities (host only)."""
+    arr = (C.c_double * max(len(sims), 1))(*[float(x) for x in sims])
+    r = lib().bc_shallow_depth(arr, len(sims), float(tau))
+    if r < 0:
+        raise BiCacheError(-1, "invalid similarities")
+    return r
+
+
+def build_depth_table(ratios, depths, n_buckets=100):
+    """Table T (host only): list of n_buckets + 1 ints, -1 where no data."""
+    n = len(ratios)
+    ra = (C.c_double * max(n, 1))(*[float(x) for x in ratios])
+    da = (C.c_int * max(n, 1))(*[int(x) for x in depths])
+    tab = (C.c_int * (n_buckets + 1))()
+    _check(lib().bc_build_depth_table(ra, da, n, n_buckets, tab))
+    return list(tab)
+
+
+def depth_lookup(table, r):
+    """d for shared-prefix ratio r from table T (host only)."""
+    ta = (C.c_int * len(table))(*[int(x) for x in table])
+    d = lib().bc_depth_lookup(ta, len(table) - 1, float(r))
+    if d < 0:
+        raise BiCacheError(-1, f"invalid lookup r={r}")
+    return d
 
 
 DEEP_MODES = {"refresh": 0, "reuse": 1}
@@ -315,6 +369,25 @@ class Model:
                                            n_s, d, _dev(out, torch.float32, "out"),
                                            C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
         return out
+
+    def profile_similarity(self, key, x_suffix, sims=None):
+        """sim_{l,1} (Eq. 3) of every request of x_suffix [B, n_s, h] (bf16,
+        device) and every layer, over the cached prefix ``key`` (all L layers
+        cached).  Returns a device fp64 tensor [B, L]."""
+        B, n_s, h = x_suffix.shape
+        got = self.lookup(key)
+        if got is None:
+            raise BiCacheError(-2, f"key {key:#x} is not cached")
+        wsb = int(lib().bc_profile_workspace_bytes(self._h, got[0], B, n_s))
+        if wsb == 0:
+            raise BiCacheError(-1, f"invalid profiling shape B={B} n_s={n_s}")
+        ws = self._workspace(wsb, x_suffix.device)
+        if sims is None:
+            sims = torch.empty((B, self.cfg["n_layers"]), dtype=torch.float64, device=x_suffix.device)
+        _check(lib().bc_profile_similarity(self._h, C.c_uint64(key), _dev(x_suffix, torch.bfloat16, "x_suffix"),
+                                           B, n_s, _dev(sims, torch.float64, "sims"),
+                                           C.c_void_p(ws.data_ptr()), ws.numel(), _stream()))
+        return sims
 
     def deep_store_bytes(self, m, B, n_s, d):
         return int(lib().bc_deep_store_bytes(self._h, m, B, n_s, d))

@@ -24,7 +24,7 @@ HOST_LIB = os.path.join(ROOT, "tests", "native", "libbicache_table_host.so")
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"
-SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "runtime.cpp", "xxh64.cpp"]
+SOURCES = ["gemm.hip", "attention.hip", "elementwise.hip", "profiling.hip", "runtime.cpp", "xxh64.cpp"]
 FLAGS = [
     "-O3", "-std=c++17", "-fPIC", f"--offload-arch={ARCH}",
     # no packed-fp32 (v_pk_*_f32) instructions anywhere in device code

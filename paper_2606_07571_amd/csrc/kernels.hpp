@@ -56,6 +56,23 @@ struct AttnArgs {
 };
 hipError_t attention(const AttnArgs& a, hipStream_t s);
 
+// ----- KV similarity (Eq. 3): out[b * out_stride] = cos(flatten(a), flatten(r_b))
+// for b < B.  Both sides are P parts x H heads x E contiguous elements (E a
+// multiple of 8): cached element (p, g, i) at a + p*a_part + g*a_head + i,
+// request b's at r + p*r_part + b*r_req + g*r_head + i (bf16).  `partial` is
+// scratch of kv_cosine_partial_bytes(v) bytes; out is fp64.
+struct CosView {
+  const void* a;
+  long a_part, a_head;
+  const void* r;
+  long r_part, r_req, r_head;
+  int P, H;
+  long E;
+  int B;
+};
+size_t kv_cosine_partial_bytes(const CosView& v);
+hipError_t kv_cosine(const CosView& v, double* partial, double* out, long out_stride, hipStream_t s);
+
 // ----- elementwise / normalisation
 // out[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gain)
 hipError_t rmsnorm(const float* x, const void* gain, void* out, int rows, int h, float eps,

@@ -11,6 +11,7 @@
 #include <stdio.h>
 
 #include <climits>
+#include <cmath>
 #include <cstdint>
 #include <new>
 #include <string>
@@ -516,6 +517,34 @@ bc_status prefix_attention(const void* q, const void* k_pre, const void* v_pre, 
   return ok();
 }
 
+
+struct ProfilePlan {
+  size_t step = 0, store = 0, out = 0, partial = 0, total = 0;
+};
+
+bc::CosView kv_view(const bc_model_config& c, int m, int B) {
+  bc::CosView v{};
+  v.P = 2;
+  v.H = c.n_kv_heads;
+  v.E = (long)m * c.head_dim;
+  v.B = B;
+  return v;
+}
+
+ProfilePlan profile_plan(const bc_model* model, int m, int B, int n_s) {
+  ProfilePlan pp;
+  const bc_model_config& c = model->cfg;
+  Bump b;
+  const size_t ws = bc_step_workspace_bytes(model, m, B, n_s, 0);
+  if (!ws) return pp;
+  pp.step = b.take(ws);
+  pp.store = b.take(deep_layout(c, m, B, n_s, 0).total);
+  pp.out = b.take((size_t)B * n_s * c.hidden * 4);
+  pp.partial = b.take(bc::kv_cosine_partial_bytes(kv_view(c, m, B)));
+  pp.total = b.at;
+  return pp;
+}
+
 }  // namespace
 
 extern "C" {
@@ -756,6 +785,114 @@ bc_status bc_step_forward_multi(bc_model* model, const uint64_t* keys, const int
   for (int g = 0; g < n_groups; ++g) gs[g] = Group{keys[g], counts[g]};
   return step_impl(model, gs.data(), n_groups, x_suffix, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out,
                    workspace, ws_bytes, stream);
+}
+
+// ------------------------------------------------------- shared-prefix profiling
+
+
+size_t bc_profile_workspace_bytes(const bc_model* model, int m, int B, int n_s) {
+  if (!model) return 0;
+  return profile_plan(model, m, B, n_s).total;
+}
+
+bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
+                                double* sims, void* workspace, size_t ws_bytes, void* stream) {
+  if (!model || !x_suffix || !sims || !workspace) return fail(BC_E_INVALID, "null argument");
+  const bc::CacheEntry* ent = model->table.find(key);
+  if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
+  const bc_model_config& c = model->cfg;
+  const int L = c.n_layers, m = ent->m;
+  if (ent->n_layers != L)
+    return fail(BC_E_INVALID, "profiling needs KV$ of all %d layers; the entry caches %d", L, ent->n_layers);
+  std::string why;
+  if (!step_shape_ok(c, m, B, n_s, 0, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  const ProfilePlan pp = profile_plan(model, m, B, n_s);
+  if (!pp.total) return fail(BC_E_INVALID, "invalid profiling shape");
+  if (ws_bytes < pp.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, pp.total);
+  if ((uintptr_t)workspace % kAlign) return fail(BC_E_INVALID, "workspace must be 256-byte aligned");
+  char* ws = (char*)workspace;
+  hipStream_t s = (hipStream_t)stream;
+  // KV^ref_{l,1}: the un-cached forward of (p, z) at the first step (d = 0),
+  // every layer's K/V of every row written to the deep store
+  const Group g{key, B};
+  bc_status st = step_impl(model, &g, 1, x_suffix, n_s, 0, BC_DEEP_REFRESH, ws + pp.store,
+                           pp.out - pp.store, (float*)(ws + pp.out), ws + pp.step, pp.store - pp.step,
+                           stream);
+  model->deep_tags.erase((uintptr_t)(ws + pp.store));
+  if (st != BC_OK) return st;
+  const EntryLayout e = entry_layout(c, m, L);
+  const DeepLayout dl = deep_layout(c, m, B, n_s, 0);
+  const char* cm = (const char*)ent->mem;
+  for (int l = 0; l < L; ++l) {
+    bc::CosView v = kv_view(c, m, B);
+    v.a = cm + (size_t)(2 * l) * e.kv_layer;   // KV$_l: K then V, [Hkv][m][dh] each
+    v.a_part = (long)(e.kv_layer / 2);
+    v.a_head = (long)m * c.head_dim;
+    v.r = ws + pp.store + (size_t)(2 * l) * dl.part;  // request b's prefix rows of layer l
+    v.r_part = (long)(dl.part / 2);
+    v.r_req = dl.sb;
+    v.r_head = dl.sh;
+    BC_LAUNCH(model, BC_K_KVSIM, s, bc::kv_cosine(v, (double*)(ws + pp.partial), sims + l, L, s));
+  }
+  return ok();
+}
+
+size_t bc_cosine_workspace_bytes(long n) {
+  if (n <= 0 || n % 8) return 0;
+  bc::CosView v{};
+  v.P = v.H = v.B = 1;
+  v.E = n;
+  return bc::kv_cosine_partial_bytes(v);
+}
+
+bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out, void* workspace,
+                               size_t ws_bytes, void* stream) {
+  if (!a || !b || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (n <= 0 || n % 8) return fail(BC_E_INVALID, "n=%ld must be a positive multiple of 8", n);
+  if ((uintptr_t)a % 16 || (uintptr_t)b % 16) return fail(BC_E_INVALID, "operands must be 16-byte aligned");
+  const size_t need = bc_cosine_workspace_bytes(n);
+  if (ws_bytes < need) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, need);
+  bc::CosView v{};
+  v.a = a;
+  v.r = b;
+  v.P = v.H = v.B = 1;
+  v.E = n;
+  BC_HIP(bc::kv_cosine(v, (double*)workspace, out, 1, (hipStream_t)stream));
+  return ok();
+}
+
+int bc_shallow_depth(const double* sims, int n_layers, double tau) {
+  if (!sims || n_layers < 0) return -1;
+  int b = 0;
+  while (b < n_layers && sims[b] >= tau) ++b;
+  return b;
+}
+
+bc_status bc_build_depth_table(const double* ratios, const int* depths, int n, int n_buckets,
+                               int* table) {
+  if (!ratios || !depths || !table || n < 0 || n_buckets < 1) return fail(BC_E_INVALID, "bad argument");
+  std::vector<long> sum(n_buckets + 1, 0), cnt(n_buckets + 1, 0);
+  for (int i = 0; i < n; ++i) {
+    const double k = ratios[i] * n_buckets;
+    const long kr = lround(k);
+    if (kr < 1 || kr > n_buckets || fabs((double)kr / n_buckets - ratios[i]) >= 1e-9)
+      return fail(BC_E_INVALID, "ratio %g of request %d is not a bucket value k/%d", ratios[i], i, n_buckets);
+    if (depths[i] < 0) return fail(BC_E_INVALID, "depth %d of request %d is negative", depths[i], i);
+    sum[kr] += depths[i];
+    cnt[kr] += 1;
+  }
+  table[0] = -1;
+  for (int k = 1; k <= n_buckets; ++k) table[k] = cnt[k] ? (int)(sum[k] / cnt[k]) : -1;
+  return ok();
+}
+
+int bc_depth_lookup(const int* table, int n_buckets, double r) {
+  if (!table || n_buckets < 1 || !(r >= 0.0)) return -1;
+  long k = (long)floor(r * n_buckets + 1e-9);
+  if (k > n_buckets) k = n_buckets;
+  for (; k >= 1; --k)
+    if (table[k] >= 0) return table[k];
+  return 0;
 }
 
 bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) {

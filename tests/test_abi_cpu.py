@@ -220,6 +220,33 @@ def test_deep_step_validation_without_device_work():
     L.bc_model_destroy(h)
 
 
+def test_depth_rule_and_table_match_oracle():
+    from oracle import profiling as P
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        L = int(rng.integers(0, 40))
+        sims = list(1 - np.abs(rng.normal(scale=0.03, size=L)))
+        tau = float(rng.choice([0.9, 0.95, 0.97, 0.99]))
+        assert bc.shallow_depth(sims, tau) == P.shallow_depth(sims, tau)
+    n_buckets = 100
+    ks = rng.integers(1, n_buckets + 1, size=500)
+    ks[ks == 37] = 38                       # leave bucket 37 without data
+    ratios = [k / n_buckets for k in ks]
+    depths = [int(x) for x in rng.integers(0, 33, size=500)]
+    T = bc.build_depth_table(ratios, depths, n_buckets)
+    assert T == P.build_table(ratios, depths, n_buckets)
+    assert T[37] == -1
+    for r in list(np.linspace(0, 1, 401)) + [0.37, 0.3699999, 0.75, 1.0]:
+        assert bc.depth_lookup(T, r) == P.lookup_depth(T, r), r
+    with pytest.raises(bc.BiCacheError):
+        bc.build_depth_table([0.333], [1], 100)
+    with pytest.raises(bc.BiCacheError):
+        bc.build_depth_table([0.5], [-1], 100)
+    L = bc.lib()
+    assert L.bc_cosine_workspace_bytes(12) == 0 and L.bc_cosine_workspace_bytes(0) == 0
+    assert L.bc_cosine_workspace_bytes(8 * 8192) > 0
+
+
 # ------------------------------------------------------------ FIFO bookkeeping
 
 @pytest.fixture(scope="module")

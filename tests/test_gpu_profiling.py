@@ -1,0 +1,127 @@
+"""GPU checks of the shared-prefix profiling primitives (Eq. 3, Sec. 4.2, 5.1).
+
+* The cosine reduction on flat bf16 vectors of ragged sizes (one element
+  vector to several workgroups with a partial chunk) against fp64 NumPy on the
+  same values; cos(a, a) = 1, cos(a, -a) = -1; repeated runs bit-identical.
+* Per-request, per-layer sim_{l,1} of a small model against the oracle's
+  profile (fp64 KVs), the first layer exactly 1 (footnote of Sec. 4.2), and
+  the depth rule applied to both.
+* Requests are independent: a request's similarities are bit-identical alone
+  or in a batch, also past 16 requests (a second reduction pass).
+* At the C3 shape (32 layers, prefix 1536, 16 requests of 512): first layer 1,
+  values in [-1, 1], request 15 alone bit-identical to its batch row.
+"""
+import numpy as np
+import pytest
+import torch
+
+from oracle import profiling as OP
+import paper_2606_07571_amd as bc
+from paper_2606_07571_amd import synth
+from paper_2606_07571_amd.synth import to_f64, weights_f64
+from tests.parity import say
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.mark.parametrize("n", [8, 64, 8192, 8200, 3 * 8192 + 24, 1_000_008])
+def test_cosine_reduction_matches_numpy(n):
+    say(f"cosine n={n}")
+    a = synth.gaussian((n,), 61000 + n % 97)
+    b = (a.float() + 0.7 * synth.gaussian((n,), 62000 + n % 89).float()).to(torch.bfloat16)
+    ad, bd = a.cuda(), b.cuda()
+    got = bc.cosine_similarity(ad, bd).item()
+    again = bc.cosine_similarity(ad, bd).item()
+    x, y = to_f64(a), to_f64(b)
+    ref = float(x @ y) / np.sqrt(float(x @ x) * float(y @ y))
+    assert abs(got - ref) <= 1e-6, (got, ref)
+    assert got == again
+    assert abs(bc.cosine_similarity(ad, ad).item() - 1.0) <= 1e-15
+    assert abs(bc.cosine_similarity(ad, (-a).cuda()).item() + 1.0) <= 1e-15
+
+
+CFG = synth.model_config(n_layers=4, hidden=256, n_heads=4, n_kv_heads=2, head_dim=64, ffn=512)
+
+
+@pytest.fixture(scope="module")
+def prof():
+    cfg = CFG
+    w_cpu = synth.model_weights(cfg, 63000)
+    w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in w_cpu]
+    model = bc.Model(cfg, w_dev, cache_capacity=4)
+    m, n_s = 96, 40
+    xp = synth.gaussian((m, cfg["hidden"]), 63100)
+    key = bc.prefix_key(np.arange(m) + 63)
+    model.populate(key, xp.cuda(), cfg["n_layers"])
+    torch.cuda.synchronize()
+    yield cfg, model, key, xp, weights_f64(w_cpu), n_s
+    model.close()
+
+
+def test_profile_matches_oracle(prof):
+    cfg, model, key, xp, w64, n_s = prof
+    B = 3
+    xs = synth.gaussian((B, n_s, cfg["hidden"]), 63200)
+    say("profile similarity, small model")
+    sims = model.profile_similarity(key, xs.cuda()).cpu().numpy()
+    assert sims.shape == (B, cfg["n_layers"])
+    for b in range(B):
+        ref = OP.profile_request(to_f64(xp), to_f64(xs[b]), w64, cfg)
+        say(f"  request {b}: gpu {np.round(sims[b], 6)} oracle {np.round(ref, 6)}")
+        assert abs(sims[b, 0] - 1.0) <= 1e-12          # first layer: identical KVs
+        np.testing.assert_allclose(sims[b], ref, atol=1e-3, rtol=0)
+        for tau in (0.9, 0.99):
+            # the rule agrees wherever no similarity sits within the tolerance of tau
+            if np.all(np.abs(ref - tau) > 2e-3):
+                assert bc.shallow_depth(sims[b], tau) == OP.shallow_depth(ref, tau)
+
+
+def test_profile_requests_independent(prof):
+    cfg, model, key, xp, w64, n_s = prof
+    B = 18                                               # two reduction passes (16 + 2)
+    xs = synth.gaussian((B, n_s, cfg["hidden"]), 63300).cuda()
+    say("profile similarity, 18 requests")
+    sims = model.profile_similarity(key, xs)
+    again = model.profile_similarity(key, xs)
+    alone = [model.profile_similarity(key, xs[b:b + 1].contiguous()) for b in (0, 16, 17)]
+    torch.cuda.synchronize()
+    assert torch.equal(sims, again)
+    for b, one in zip((0, 16, 17), alone):
+        assert torch.equal(one[0], sims[b]), f"request {b}"
+
+
+def test_profile_needs_every_layer_cached(prof):
+    cfg, model, key, xp, w64, n_s = prof
+    part = bc.prefix_key(np.arange(50) + 6400)
+    model.populate(part, synth.gaussian((50, cfg["hidden"]), 63400).cuda(), 2)
+    torch.cuda.synchronize()
+    with pytest.raises(bc.BiCacheError) as e:
+        model.profile_similarity(part, synth.gaussian((1, n_s, cfg["hidden"]), 1).cuda())
+    assert e.value.status == -1
+    model.invalidate(part)
+
+
+def test_c3_shape_profile():
+    cfg = synth.model_config()
+    sc = synth.STEP_CONFIG
+    B, m, n_s = sc["B"], sc["m"], sc["n_s"]
+    say("C3 profile: weights")
+    weights = synth.model_weights(cfg, 64000, device="cuda")
+    xp, xs = synth.step_inputs(cfg, B, m, n_s, 64500, device="cuda")
+    model = bc.Model(cfg, weights, cache_capacity=1)
+    try:
+        key = bc.prefix_key(range(m))
+        model.populate(key, xp, cfg["n_layers"])
+        say("C3 profile: 16 requests x 32 layers")
+        sims = model.profile_similarity(key, xs)
+        one = model.profile_similarity(key, xs[B - 1:].contiguous())
+        torch.cuda.synchronize()
+        s = sims.cpu().numpy()
+        say(f"  mean sim per layer: {np.round(s.mean(0), 4)}")
+        assert np.all(np.abs(s[:, 0] - 1.0) <= 1e-12)
+        assert np.all(np.isfinite(s)) and np.all(s <= 1.0 + 1e-12) and np.all(s >= -1.0)
+        assert torch.equal(one[0], sims[B - 1])
+    finally:
+        model.close()
+        del weights
+        torch.cuda.empty_cache()
