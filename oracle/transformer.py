@@ -86,16 +86,20 @@ def project_qkv(x_res, lw, cfg, positions):
     """RMSNorm, then the Q/K/V projections (Eq. 1), then RoPE on q and k.
 
     x_res: [n, h] residual rows.  w_qkv rows are [Hq*dh query | Hkv*dh key |
-    Hkv*dh value], each block head-major.  Returns q [Hq, n, dh],
-    k [Hkv, n, dh], v [Hkv, n, dh].
+    Hkv*dh value], each block head-major.  An optional bias lw["b_qkv"] (same
+    row order; the Q/K/V bias of Qwen2-style models such as Dream-7B) is added
+    to the projections before RoPE.  Returns q [Hq, n, dh], k [Hkv, n, dh],
+    v [Hkv, n, dh].
     """
     Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
     n = x_res.shape[0]
     a = rms_norm(x_res, lw["attn_norm"], cfg["rms_eps"])
-    w = lw["w_qkv"]
-    q = (a @ w[: Hq * dh].T).reshape(n, Hq, dh).transpose(1, 0, 2)
-    k = (a @ w[Hq * dh: (Hq + Hkv) * dh].T).reshape(n, Hkv, dh).transpose(1, 0, 2)
-    v = (a @ w[(Hq + Hkv) * dh:].T).reshape(n, Hkv, dh).transpose(1, 0, 2)
+    proj = a @ lw["w_qkv"].T
+    if lw.get("b_qkv") is not None:
+        proj = proj + lw["b_qkv"]
+    q = proj[:, : Hq * dh].reshape(n, Hq, dh).transpose(1, 0, 2)
+    k = proj[:, Hq * dh: (Hq + Hkv) * dh].reshape(n, Hkv, dh).transpose(1, 0, 2)
+    v = proj[:, (Hq + Hkv) * dh:].reshape(n, Hkv, dh).transpose(1, 0, 2)
     q = rope(q, positions, cfg["rope_theta"])
     k = rope(k, positions, cfg["rope_theta"])
     return q, k, v

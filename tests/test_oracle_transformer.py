@@ -98,8 +98,9 @@ def _layer_loops(x, lw, cfg, pos):
         r = math.sqrt(sum(t * t for t in row) / h + eps)
         return [row[i] / r * g[i] for i in range(h)]
 
-    def matvec(W, a, r0, nr):
-        return [sum(W[r0 + r][c] * a[c] for c in range(len(a))) for r in range(nr)]
+    def matvec(W, a, r0, nr, bias=None):
+        return [sum(W[r0 + r][c] * a[c] for c in range(len(a))) + (bias[r0 + r] if bias else 0.0)
+                for r in range(nr)]
 
     def rot(vec, p):
         out = list(vec)
@@ -113,9 +114,10 @@ def _layer_loops(x, lw, cfg, pos):
     Q, K, V = [], [], []
     for t in range(n):
         a = norm(x[t], lw["attn_norm"])
-        Q.append([rot(matvec(lw["w_qkv"], a, hd * dh, dh), pos[t]) for hd in range(Hq)])
-        K.append([rot(matvec(lw["w_qkv"], a, (Hq + g) * dh, dh), pos[t]) for g in range(Hkv)])
-        V.append([matvec(lw["w_qkv"], a, (Hq + Hkv + g) * dh, dh) for g in range(Hkv)])
+        bq = lw.get("b_qkv")
+        Q.append([rot(matvec(lw["w_qkv"], a, hd * dh, dh, bq), pos[t]) for hd in range(Hq)])
+        K.append([rot(matvec(lw["w_qkv"], a, (Hq + g) * dh, dh, bq), pos[t]) for g in range(Hkv)])
+        V.append([matvec(lw["w_qkv"], a, (Hq + Hkv + g) * dh, dh, bq) for g in range(Hkv)])
     out = []
     for t in range(n):
         o = []
@@ -145,6 +147,29 @@ def test_layer_against_loops():
     lw_list = {k: v.tolist() for k, v in lw.items()}
     ref = _layer_loops(x.tolist(), lw_list, cfg, pos.tolist())
     np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+
+
+def test_layer_with_qkv_bias_against_loops():
+    """Q/K/V bias (Qwen2-style layers such as Dream-7B's): added to the
+    projections before RoPE; GQA with a group of 3."""
+    cfg = _cfg(n_layers=1, hidden=8, n_heads=3, n_kv_heads=1, head_dim=4, ffn=6)
+    rng = np.random.default_rng(12)
+    lw = _weights(cfg, rng)[0]
+    lw["b_qkv"] = rng.normal(size=(5 * 4,))
+    x = rng.normal(size=(3, 8))
+    pos = np.array([2, 9, 4])
+    got, _, _ = T.layer_full(x, lw, cfg, pos)
+    lw_list = {k: v.tolist() for k, v in lw.items()}
+    ref = _layer_loops(x.tolist(), lw_list, cfg, pos.tolist())
+    np.testing.assert_allclose(got, ref, rtol=1e-12, atol=1e-12)
+    # the bias matters, and with zero weights the projections are the bias itself
+    assert np.abs(got - T.layer_full(x, {**lw, "b_qkv": None}, cfg, pos)[0]).max() > 1e-6
+    zero = {**lw, "w_qkv": np.zeros_like(lw["w_qkv"])}
+    q, k, v = T.project_qkv(x, zero, cfg, pos)
+    np.testing.assert_allclose(v[0], np.tile(lw["b_qkv"][16:20], (3, 1)), atol=1e-15)
+    # position 0 leaves q unrotated
+    q0, _, _ = T.project_qkv(x[:1], zero, cfg, np.array([0]))
+    np.testing.assert_allclose(q0[:, 0], lw["b_qkv"][:12].reshape(3, 4), atol=1e-15)
 
 
 # ---------------------------------------------------------------- step
