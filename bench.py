@@ -18,8 +18,8 @@ HIP events inside the timed region, the fp64 CPU oracle timed on a bounded
 sample (rank 0), plus the per-depth step times, the deep-layer reuse steps of
 Eq. 5 (refresh, reuse, and their mix at refresh interval 16), the profiling
 pass of Eq. 3 (KV similarity of every request and layer), a batch over four
-prefixes of different lengths, and the shared-prefix attention throughput of
-the attention-only workloads.
+prefixes of different lengths, the shared-prefix attention throughput of the
+attention-only workloads, and the full step at the Dream-7B shape (GQA).
 """
 import argparse
 import json
@@ -310,6 +310,35 @@ def main():
                                 "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
         del ins, o
 
+    # ---------------------------------------------------------------- Dream-7B-shaped full step
+    # 28 layers, GQA 28/4 x 128, hidden 3584, SwiGLU 18944, Q/K/V bias; the GQA
+    # workload's sizes: 64 requests, shared prefix 1024, suffix 384
+    dcfg = synth.dream_config()
+    ds = synth.DREAM_STEP
+    dB, dm, dn = ds["B"], ds["m"], ds["n_s"]
+    log(f"bench: Dream-7B-shaped step ({dcfg})")
+    dweights = synth.model_weights(dcfg, 8000, device=dev)
+    dxp, dxs = synth.step_inputs(dcfg, dB, dm, dn, 8500, device=dev)
+    dmodel = bc.Model(dcfg, dweights, cache_capacity=1)
+    dkey = bc.prefix_key(range(dm))
+    dmodel.populate(dkey, dxp, dcfg["n_layers"])
+    dout = torch.empty((dB, dn, dcfg["hidden"]), dtype=torch.float32, device=dev)
+    dream = {"model": "Dream-7B shape (28 layers, 28/4 x 128 heads, h 3584, F 18944, QKV bias)",
+             "B": dB, "prefix": dm, "suffix": dn}
+    d0_ms = None
+    for dd in (0, 8):
+        t = timed(lambda: dmodel.step(dkey, dxs, dd, out=dout), args.depth_steps)
+        fl = step_flops(dcfg, dB, dm, dn, dd)
+        if dd == 0:
+            d0_ms = t
+        dream[f"d{dd}"] = {"ms": round(t, 3), "request_steps_per_s": round(dB / (t / 1e3), 2),
+                           "tflops": round(fl / (t / 1e3) / 1e12, 1),
+                           "speedup_vs_d0": round(d0_ms / t, 3),
+                           "ideal_speedup": round(step_flops(dcfg, dB, dm, dn, 0) / fl, 3)}
+    dmodel.close()
+    del dweights, dmodel, dxp, dxs, dout
+    torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- CPU oracle baseline
     cpu = None
     if not args.no_cpu_baseline:
@@ -343,6 +372,7 @@ def main():
         "profiling": profiling,
         "kernel_ms_one_step": breakdown,
         "attention": attention,
+        "dream_step": dream,
         "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},
     }
     print(json.dumps(line), flush=True)

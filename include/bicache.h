@@ -28,8 +28,9 @@
  *   - A bc_model is not thread-safe: calls on one model must not overlap.
  *
  * The layer is a pre-norm transformer block: RMSNorm, fused Q/K/V projection
- * (Eq. 1), rotate-half RoPE, unmasked attention (Eq. 2), output projection
- * plus residual, RMSNorm, SwiGLU FFN plus residual, no biases.  The residual
+ * (Eq. 1, optionally with a bias), rotate-half RoPE, unmasked attention
+ * (Eq. 2), output projection plus residual, RMSNorm, SwiGLU FFN plus
+ * residual; no other biases.  The residual
  * stream is fp32; GEMM and attention operands are bf16 with fp32
  * accumulation.
  */
@@ -79,6 +80,9 @@ typedef struct {
  *           ffn(x) = w_down (silu(gate x) * (up x)).
  * w_down    [h, F]
  * attn_norm, ffn_norm [h]: RMSNorm gains.
+ * b_qkv     [(Hq + 2*Hkv)*dh] or NULL: bias of the Q/K/V projection, same row
+ *           order as w_qkv, added before RoPE (Qwen2-style layers, e.g.
+ *           Dream-7B); NULL for none.
  * The weights are referenced, not copied, and must outlive the model. */
 typedef struct {
   const void* w_qkv;
@@ -87,6 +91,7 @@ typedef struct {
   const void* w_down;
   const void* attn_norm;
   const void* ffn_norm;
+  const void* b_qkv;
 } bc_layer_weights;
 
 typedef struct bc_model bc_model;

@@ -32,7 +32,8 @@ class ModelConfig(C.Structure):
 
 class LayerWeights(C.Structure):
     _fields_ = [("w_qkv", C.c_void_p), ("w_o", C.c_void_p), ("w_gate_up", C.c_void_p),
-                ("w_down", C.c_void_p), ("attn_norm", C.c_void_p), ("ffn_norm", C.c_void_p)]
+                ("w_down", C.c_void_p), ("attn_norm", C.c_void_p), ("ffn_norm", C.c_void_p),
+                ("b_qkv", C.c_void_p)]
 
 
 _SIGS = {
@@ -246,6 +247,8 @@ class Model:
         for i, lw in enumerate(layers):
             for k in _WEIGHT_KEYS:
                 setattr(arr[i], k, lw[k].data_ptr() if lw[k] is not None else None)
+            bias = lw.get("b_qkv")
+            arr[i].b_qkv = bias.data_ptr() if bias is not None else None
         h = C.c_void_p()
         _check(lib().bc_model_create(C.byref(c), arr, cache_capacity, C.byref(h)))
         self._h = h

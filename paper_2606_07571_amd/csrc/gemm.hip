@@ -1,6 +1,7 @@
 // bf16 GEMMs on gfx950 MFMA with the epilogues of the transformer layer:
 // residual add (O and down projections), SwiGLU (gate/up projection) and the
-// fused Q/K/V projection with rotate-half RoPE and head-major scatter (which,
+// fused Q/K/V projection with optional bias, rotate-half RoPE and head-major
+// scatter (which,
 // during populate, writes the prefix K/V straight into the cache entry).
 //
 // C[M, N] = A[M, K] . W[N, K]^T.  Both operands are K-contiguous, so every
@@ -140,6 +141,7 @@ struct EpiQKV {
   int Hq, Hkv, n_seq, pos0;
   const float* cos_t;
   const float* sin_t;
+  const bf16* bias;  // [(Hq + 2*Hkv) * DH] added before RoPE, or null
   __host__ __device__ int ncols() const { return (Hq + 2 * Hkv) * DH; }
   __host__ __device__ int tiles_n(int BN) const { return cdiv(ncols(), BN); }
   template <int BN, int TN>
@@ -180,8 +182,12 @@ struct EpiQKV {
 #pragma unroll
           for (int jj = 0; jj < BPH / 2; ++jj) {
             const int d1 = jj * 32 + (lane & 31);
-            const float x1 = acc[i][hh * BPH + jj][e];
-            const float x2 = acc[i][hh * BPH + jj + BPH / 2][e];
+            float x1 = acc[i][hh * BPH + jj][e];
+            float x2 = acc[i][hh * BPH + jj + BPH / 2][e];
+            if (bias) {
+              x1 += bf16_to_f32(bias[head_g * DH + d1]);
+              x2 += bf16_to_f32(bias[head_g * DH + d1 + DH / 2]);
+            }
             float y1 = x1, y2 = x2;
             if (rot) {
               const float c = ct[d1], s = st[d1];
@@ -499,11 +505,11 @@ hipError_t gemm_qkv_rope(const void* A, int lda, const void* W, int ldw, int M, 
   GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K};
   if (dh == 128) {
     EpiQKV<128> e{(bf16*)o.q, (bf16*)o.k, (bf16*)o.v, o.q_sb, o.q_sh, o.k_sb, o.k_sh,
-                  o.v_sb, o.v_sh, Hq, Hkv, n_seq, pos0, cos_t, sin_t};
+                  o.v_sb, o.v_sh, Hq, Hkv, n_seq, pos0, cos_t, sin_t, (const bf16*)o.bias};
     return launch(a, e, s);
   }
   EpiQKV<64> e{(bf16*)o.q, (bf16*)o.k, (bf16*)o.v, o.q_sb, o.q_sh, o.k_sb, o.k_sh,
-               o.v_sb, o.v_sh, Hq, Hkv, n_seq, pos0, cos_t, sin_t};
+               o.v_sb, o.v_sh, Hq, Hkv, n_seq, pos0, cos_t, sin_t, (const bf16*)o.bias};
   return launch(a, e, s);
 }
 

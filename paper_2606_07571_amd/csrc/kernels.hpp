@@ -22,13 +22,15 @@ hipError_t gemm_swiglu(const void* A, int lda, const void* W, int ldw, int M, in
 // t = r % n_seq of sequence b = r / n_seq at position pos0 + t.  Output column
 // block j of W (head j, dh rows) goes to Q head j (j < Hq), K head j - Hq
 // (j < Hq + Hkv) or V head j - Hq - Hkv; element (b, head, t, dim) of a part is
-// stored at base + b*sb + head*sh + t*dh + dim (bf16).  Q and K are rotated
-// with the tables cos_t/sin_t [pos][dh/2].
+// stored at base + b*sb + head*sh + t*dh + dim (bf16).  The bias (bf16, one
+// per output column, or null) is added first; Q and K are then rotated with
+// the tables cos_t/sin_t [pos][dh/2].
 struct QkvOut {
   void* q;
   void* k;
   void* v;
   long q_sb, q_sh, k_sb, k_sh, v_sb, v_sh;
+  const void* bias = nullptr;
 };
 hipError_t gemm_qkv_rope(const void* A, int lda, const void* W, int ldw, int M, int K, int Hq,
                          int Hkv, int dh, int n_seq, int pos0, const float* cos_t,

@@ -248,7 +248,7 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
     const int seg_rows = g.n_req * g.n_seq;
     uint16_t* qg = q + g.row0 * hd;
     bc::QkvOut qo{qg, g.k_dst, g.v_dst, (long)Hq * g.n_seq * dh, (long)g.n_seq * dh,
-                  g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh};
+                  g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh, w.b_qkv};
     BC_LAUNCH(mdl, BC_K_QKV, s,
               bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, seg_rows, h, Hq, Hkv, dh, g.n_seq,
                                 g.pos0, cos_t, sin_t, qo, s));

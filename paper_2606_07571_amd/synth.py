@@ -47,10 +47,23 @@ ATTN_CONFIGS = {
 
 
 def model_config(n_layers=32, hidden=4096, n_heads=32, n_kv_heads=32, head_dim=128,
-                 ffn=12288, rms_eps=1e-5, rope_theta=500000.0):
+                 ffn=12288, rms_eps=1e-5, rope_theta=500000.0, qkv_bias=False):
     """The C3 layer shape by default (hidden 4096, 32 x 128 heads, SwiGLU 12288)."""
     return dict(n_layers=n_layers, hidden=hidden, n_heads=n_heads, n_kv_heads=n_kv_heads,
-                head_dim=head_dim, ffn=ffn, rms_eps=rms_eps, rope_theta=rope_theta)
+                head_dim=head_dim, ffn=ffn, rms_eps=rms_eps, rope_theta=rope_theta,
+                qkv_bias=qkv_bias)
+
+
+def dream_config(n_layers=28):
+    """The Dream-7B shape (its Qwen2.5-7B base: hidden 3584, 28 query and 4 KV
+    heads of 128, SwiGLU 18944, Q/K/V bias, RMSNorm eps 1e-6, RoPE base 1e6)."""
+    return model_config(n_layers=n_layers, hidden=3584, n_heads=28, n_kv_heads=4, head_dim=128,
+                        ffn=18944, rms_eps=1e-6, rope_theta=1000000.0, qkv_bias=True)
+
+
+# Full step of the Dream-7B shape over the GQA workload's sizes: 64 requests,
+# shared prefix 1024, suffix 384.
+DREAM_STEP = dict(B=64, m=1024, n_s=384)
 
 
 STEP_CONFIG = dict(B=16, m=1536, n_s=512, depths=(0, 4, 8, 16))
@@ -93,7 +106,7 @@ def layer_weights(cfg, layer, seed_base, device="cpu"):
 
     Q/K/V, gate and up ~ N(0, 1/fan_in); W_o and W_down ~ N(0, 1/fan_in)/sqrt(2L)
     (depth-scaled so that the fp32 residual stream stays O(1) over 32 layers);
-    norm gains 1 + N(0, 0.1^2).
+    norm gains 1 + N(0, 0.1^2); with cfg["qkv_bias"], a Q/K/V bias ~ N(0, 0.1^2).
     """
     h, F, L = cfg["hidden"], cfg["ffn"], cfg["n_layers"]
     Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
@@ -106,6 +119,8 @@ def layer_weights(cfg, layer, seed_base, device="cpu"):
         "w_down": gaussian((h, F), base + 3, depth / math.sqrt(F), device=device),
         "attn_norm": gaussian((h,), base + 4, 0.1, mean=1.0, device=device),
         "ffn_norm": gaussian((h,), base + 5, 0.1, mean=1.0, device=device),
+        "b_qkv": (gaussian(((Hq + 2 * Hkv) * dh,), seed_base + 10_000_000 + layer, 0.1, device=device)
+                  if cfg.get("qkv_bias") else None),
     }
 
 
@@ -127,7 +142,7 @@ def to_f64(t):
 
 
 def weights_f64(layers):
-    return [{k: to_f64(v) for k, v in lw.items()} for lw in layers]
+    return [{k: (to_f64(v) if v is not None else None) for k, v in lw.items()} for lw in layers]
 
 
 def denoise_inputs(cfg, T, B, n_s, n_gen, per_step, seed_base, device="cpu"):
@@ -152,3 +167,8 @@ def denoise_inputs(cfg, T, B, n_s, n_gen, per_step, seed_base, device="cpu"):
         if lo < hi:
             x[:, lo:hi] = fresh[t, :, :hi - lo]
     return torch.stack(out).to(torch.bfloat16).to(device)
+
+
+def to_device(layers, device="cuda"):
+    """Copy per-layer weight dicts to the device (absent entries stay None)."""
+    return [{k: (v.to(device) if v is not None else None) for k, v in lw.items()} for lw in layers]

@@ -33,7 +33,7 @@ def test_c3_layer_shape_every_depth():
     cfg = synth.model_config(n_layers=2)
     B, m, n_s = 2, 128, 64
     w_cpu = synth.model_weights(cfg, 31000)
-    w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in w_cpu]
+    w_dev = synth.to_device(w_cpu)
     xp, xs = synth.step_inputs(cfg, B, m, n_s, 31500)
     model = bc.Model(cfg, w_dev, cache_capacity=2)
     try:
@@ -108,7 +108,7 @@ def test_c4_populate_first_layer_sampled():
     h, Hkv, dh = cfg["hidden"], cfg["n_kv_heads"], cfg["head_dim"]
     L = synth.POPULATE_C4["n_layers_to_cache"]
     w_cpu = synth.model_weights(cfg, 41000)
-    w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in w_cpu]
+    w_dev = synth.to_device(w_cpu)
     xp = synth.gaussian((m, h), 41500)
     model = bc.Model(cfg, w_dev, cache_capacity=1)
     try:

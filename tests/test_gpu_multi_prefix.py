@@ -32,7 +32,7 @@ N_S = 65
 def multi():
     cfg = CFG
     w_cpu = synth.model_weights(cfg, 51000)
-    w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in w_cpu]
+    w_dev = synth.to_device(w_cpu)
     w64 = weights_f64(w_cpu)
     model = bc.Model(cfg, w_dev, cache_capacity=8)
     keys, caches = [], []

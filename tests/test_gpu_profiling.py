@@ -47,7 +47,7 @@ CFG = synth.model_config(n_layers=4, hidden=256, n_heads=4, n_kv_heads=2, head_d
 def prof():
     cfg = CFG
     w_cpu = synth.model_weights(cfg, 63000)
-    w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in w_cpu]
+    w_dev = synth.to_device(w_cpu)
     model = bc.Model(cfg, w_dev, cache_capacity=4)
     m, n_s = 96, 40
     xp = synth.gaussian((m, cfg["hidden"]), 63100)

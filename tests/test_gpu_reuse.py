@@ -101,7 +101,7 @@ class Seq:
         self.cfg = cfg
         m, B, n_s = spec["m"], spec["B"], spec["n_s"]
         self.w_cpu = synth.model_weights(cfg, 1000 * spec["seed"])
-        self.w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in self.w_cpu]
+        self.w_dev = synth.to_device(self.w_cpu)
         self.xp = synth.gaussian((m, cfg["hidden"]), 1000 * spec["seed"] + 400)
         self.xsteps = synth.denoise_inputs(cfg, T_STEPS, B, n_s, spec["n_gen"], PER_STEP,
                                            1000 * spec["seed"] + 500)

@@ -32,7 +32,7 @@ class Setup:
         cfg = spec["cfg"]
         self.cfg = cfg
         self.w_cpu = synth.model_weights(cfg, 1000 * spec["seed"])
-        self.w_dev = [{k: v.cuda() for k, v in lw.items()} for lw in self.w_cpu]
+        self.w_dev = synth.to_device(self.w_cpu)
         self.xp, self.xs = synth.step_inputs(cfg, spec["B"], spec["m"], spec["n_s"], 1000 * spec["seed"] + 500)
         self.w64 = weights_f64(self.w_cpu)
         self.model = bc.Model(cfg, self.w_dev, cache_capacity=4)
@@ -116,7 +116,7 @@ def test_requests_independent_on_gpu(setup):
 
 def test_store_fifo_invalidate_and_errors():
     cfg = synth.model_config(n_layers=2, hidden=256, n_heads=4, n_kv_heads=4, head_dim=64, ffn=256)
-    w = [{k: v.cuda() for k, v in lw.items()} for lw in synth.model_weights(cfg, 77)]
+    w = synth.to_device(synth.model_weights(cfg, 77))
     model = bc.Model(cfg, w, cache_capacity=2)
     ref = FifoTable(2)
     xp = synth.gaussian((40, 256), 1).cuda()
