@@ -8,14 +8,12 @@
 // MFMA operand fragment is one 16-byte LDS read per lane and no transpose is
 // needed anywhere.
 //
-// Tiling: a workgroup computes a BM x BN tile with WM x WN waves; each wave
-// owns a (BM/WM) x (BN/WN) sub-tile made of 32x32 MFMA blocks
-// (v_mfma_f32_32x32x16_bf16).  K advances in steps of 64 through a
-// double-buffered LDS ring fed through registers: step k+1's tiles are written
-// to the other LDS buffer halfway through step k's MFMAs and step k+2's global
-// loads are issued right after, with one barrier per step.  LDS rows are 128 bytes
-// (64 bf16) with an XOR-swizzled 16-byte chunk index (see swz), conflict-free
-// for both the fills and the fragment reads.
+// Tiling: a workgroup computes a 256 x 256 tile with 8 waves, each a 64 x 128
+// sub-tile of 32x32 MFMA blocks (v_mfma_f32_32x32x16_bf16); K advances in
+// steps of 64 through a double-buffered LDS tile pair (see gemm_pp_kernel for
+// the schedule).  LDS rows are 128 bytes (64 bf16) with an XOR-swizzled
+// 16-byte chunk index (see swz), conflict-free for both the fills and the
+// fragment reads.
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -32,6 +30,7 @@ struct GemmArgs {
   const bf16* W;
   int ldw;
   int M, K;
+  int w_bytes;  // bytes of W that an epilogue's rows span (its buffer range)
 };
 
 // LDS serves 128-bit accesses 16 lanes (256 bytes, 64 banks) at a time; with
@@ -53,6 +52,7 @@ struct EpiResidual {
   int ldr, N;
   static constexpr bool kInit = true;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(N, BN); }
+  __host__ __device__ int w_rows() const { return N; }
   template <int BN, int TN>
   __device__ __forceinline__ int w_row(int tn, int r) const {
     int n = tn * BN + r;
@@ -102,6 +102,7 @@ struct EpiSwiGLU {
   int F;
   static constexpr bool kInit = false;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(F, BN / 2); }
+  __host__ __device__ int w_rows() const { return 2 * F; }
   template <int BN, int TN>
   __device__ __forceinline__ int w_row(int tn, int r) const {
     const int wn = r / TN, q = r % TN;
@@ -144,6 +145,7 @@ struct EpiQKV {
   const bf16* bias;  // [(Hq + 2*Hkv) * DH] added before RoPE, or null
   __host__ __device__ int ncols() const { return (Hq + 2 * Hkv) * DH; }
   __host__ __device__ int tiles_n(int BN) const { return cdiv(ncols(), BN); }
+  __host__ __device__ int w_rows() const { return ncols(); }
   template <int BN, int TN>
   __device__ __forceinline__ int w_row(int tn, int r) const {
     int n = tn * BN + r;
@@ -202,160 +204,39 @@ struct EpiQKV {
   }
 };
 
-// ---------------------------------------------------------------- kernel
-
-template <int BM, int BN, int WM, int WN, class Epi>
-__global__ void __launch_bounds__(WM * WN * kWave) gemm_kernel(GemmArgs a, Epi epi) {
-  constexpr int NT = WM * WN * kWave;
-  constexpr int TM = BM / WM, TN = BN / WN;
-  constexpr int FM = TM / 32, FN = TN / 32;
-  constexpr int A_PER = BM * BK / 8 / NT;  // 16-byte chunks per thread per step
-  constexpr int B_PER = BN * BK / 8 / NT;
-  static_assert(A_PER * NT * 8 == BM * BK && B_PER * NT * 8 == BN * BK, "tile/thread mismatch");
-
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
-
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-  const int wm = wave / WN, wn = wave % WN;
-
-  // tile order: XCD-contiguous, then groups of 8 row-tiles swept column-major
-  const int tiles_m = cdiv(a.M, BM), tiles_n = epi.tiles_n(BN);
-  const int lid = xcd_remap(blockIdx.x, gridDim.x);
-  constexpr int GM = 8;
-  const int per_group = GM * tiles_n;
-  const int first_m = (lid / per_group) * GM;
-  const int gsz = min(tiles_m - first_m, GM);
-  const int tm = first_m + (lid % per_group) % gsz;
-  const int tn = (lid % per_group) / gsz;
-  const int m0 = tm * BM;
-
-  // per-thread chunk sources: chunk p covers tile row tid/8 + p*NT/8, column chunk tid%8
-  const int kc = tid & 7;
-  const bf16* a_src[A_PER];
-  bool a_ok[A_PER];
-#pragma unroll
-  for (int p = 0; p < A_PER; ++p) {
-    const int r = (tid >> 3) + p * (NT / 8);
-    const int gr = m0 + r;
-    a_ok[p] = gr < a.M;
-    a_src[p] = a.A + (long)(a_ok[p] ? gr : 0) * a.lda + kc * 8;
-  }
-  const bf16* b_src[B_PER];
-  bool b_ok[B_PER];
-#pragma unroll
-  for (int p = 0; p < B_PER; ++p) {
-    const int r = (tid >> 3) + p * (NT / 8);
-    const int wr = epi.template w_row<BN, TN>(tn, r);
-    b_ok[p] = wr >= 0;
-    b_src[p] = a.W + (long)(b_ok[p] ? wr : 0) * a.ldw + kc * 8;
-  }
-
-  u32x4 ra[A_PER], rb[B_PER];
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  // Loads are unconditional (an invalid row reads the clamped row 0, always in
-  // bounds) so that no load sits behind a divergent branch; rows outside the
-  // matrix are zeroed only when the registers are written to LDS, after the
-  // current step's MFMAs, so the load latency stays hidden behind them.
-  auto fetch = [&](int k0) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < A_PER; ++p) ra[p] = *reinterpret_cast<const u32x4*>(a_src[p] + k0);
-#pragma unroll
-    for (int p = 0; p < B_PER; ++p) rb[p] = *reinterpret_cast<const u32x4*>(b_src[p] + k0);
-  };
-  auto stash = [&](int buf) __attribute__((always_inline)) {
-#pragma unroll
-    for (int p = 0; p < A_PER; ++p) {
-      const int r = (tid >> 3) + p * (NT / 8);
-      *reinterpret_cast<u32x4*>(&sA[buf][swz(r, kc)]) = a_ok[p] ? ra[p] : zero4;
-    }
-#pragma unroll
-    for (int p = 0; p < B_PER; ++p) {
-      const int r = (tid >> 3) + p * (NT / 8);
-      *reinterpret_cast<u32x4*>(&sB[buf][swz(r, kc)]) = b_ok[p] ? rb[p] : zero4;
-    }
-  };
-
-  f32x16 acc[FM][FN];
-#pragma unroll
-  for (int i = 0; i < FM; ++i)
-#pragma unroll
-    for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
-
-  if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
-  const int ksteps = a.K / BK;
-  auto compute = [&](int cur, int kk0, int kk1) __attribute__((always_inline)) {
-#pragma unroll
-    for (int kk = kk0; kk < kk1; ++kk) {
-      const int kci = kk * 2 + (lane >> 5);
-      bf16x8 af[FM], bfr[FN];
-#pragma unroll
-      for (int i = 0; i < FM; ++i) {
-        const int r = wm * TM + i * 32 + (lane & 31);
-        af[i] = *reinterpret_cast<const bf16x8*>(&sA[cur][swz(r, kci)]);
-      }
-#pragma unroll
-      for (int j = 0; j < FN; ++j) {
-        const int r = wn * TN + j * 32 + (lane & 31);
-        bfr[j] = *reinterpret_cast<const bf16x8*>(&sB[cur][swz(r, kci)]);
-      }
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(af[i], bfr[j], acc[i][j]);
-    }
-  };
-
-  // Pipeline: the registers hold step ks+1 while step ks computes; they are
-  // written to the other LDS buffer halfway through step ks (that buffer was
-  // last read in step ks-1, before the previous barrier), and step ks+2 is
-  // fetched right after, so its loads have a whole step to arrive and the LDS
-  // writes overlap the second half of the step's MFMAs.
-  fetch(0);
-  stash(0);
-  if (ksteps > 1) fetch(BK);
-  __syncthreads();
-
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int cur = ks & 1;
-    compute(cur, 0, BK / 32);
-    if (ks + 1 < ksteps) {
-      stash(cur ^ 1);
-      if (ks + 2 < ksteps) fetch((ks + 2) * BK);
-    }
-    compute(cur, BK / 32, BK / 16);
-    __syncthreads();
-  }
-
-  epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
-}
-
 // ---------------------------------------------------------------- ping-pong kernel
 // Same 256 x 256 tile and 64 x 128 wave sub-tiles, but the two waves that
 // share a SIMD never do the same kind of work at the same time.  Waves 0-3
 // (group 0, columns 0-127 of the tile) and waves 4-7 (group 1, columns
 // 128-255) run the same program, group 1 one barrier-phase behind.  Each half
 // K step (32 of K) is a memory phase -- read this half step's fragments from
-// LDS, and in the second half also write the next K step's tile to LDS and
-// issue the global loads of the one after it -- then a compute phase of 16
-// MFMAs, with a workgroup barrier between phases.  While one group issues its
-// MFMAs the other group's LDS and global traffic runs, so the matrix pipe of
-// every SIMD is fed alternately by its two waves.
+// LDS, write half of the next K step's tile into the free LDS buffer and
+// issue the global loads of the same half of the K step after it -- then a
+// compute phase of 16 MFMAs, with a workgroup barrier between phases.  While
+// one group issues its MFMAs the other group's LDS and global traffic runs,
+// so the matrix pipe of every SIMD is fed alternately by its two waves, and
+// both memory phases carry the same load.
 //
-// LDS tiles are double-buffered: K step k+1 is written during the second half
-// of step k (after every wave has finished reading that buffer's previous
-// tile, step k-1, one phase earlier for group 1) and is first read at step
-// k+1.  Group 0 fetches and writes the A tile, group 1 the W tile, 8 chunks of
-// 16 bytes per lane per K step; each fetch has a whole K step to land.
+// LDS tiles are double-buffered: K step k+1 is written during step k (after
+// every wave has finished reading that buffer's previous tile, step k-1) and
+// is first read at step k+1.  Group 0 fetches and writes the A tile, group 1
+// the W tile, 8 chunks of 16 bytes per lane per K step, through buffer loads:
+// A's descriptor starts at the tile's first row and covers its valid rows, W
+// rows that an epilogue maps to nothing get an offset past W's end, so rows
+// outside the matrices read as zero with no selects.  Each load has four
+// phases (one K step) to land before its chunk is written to LDS.
 template <class Epi>
 __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
   constexpr int BM = 256, BN = 256, TM = 64, TN = 128, FM = 2, FN = 4;
-  constexpr int PER = 8;  // 16-byte chunks per lane per K step
+  constexpr int PER = 8, HPER = 4;  // 16-byte chunks per lane per K step, per half
+  constexpr int RSRC_W3 = 0x00020000;  // raw buffer, 32-bit dwords (gfx9 family)
+  constexpr uint32_t kNoRow = 0x80000000u;  // offset past every descriptor's range
 
   __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
   __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
 
-  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int tid = threadIdx.x, lane = tid & 63;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int grp = wave >> 2;          // 0: loads A, computes columns 0-127; 1: W, 128-255
   const int wm = wave & 3, wn = grp;  // the two waves on a SIMD are w and w + 4
 
@@ -369,38 +250,42 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
   const int tn = (lid % per_group) / gsz;
   const int m0 = tm * BM;
 
-  // this lane's chunks of its group's operand tile: chunk q = lane + 64*wm + 256*p
-  // covers tile row q / 8, 16-byte column chunk q % 8
+  // this lane's chunks of its group's operand tile: chunk p covers tile row
+  // lane/8 + 8*wm + 32*p, 16-byte column chunk lane%8
   const int kc = lane & 7;
-  const bf16* src[PER];
-  bool ok[PER];
+  uint32_t voff[PER];
+  __amdgpu_buffer_rsrc_t rsrc;
+  if (grp == 0) {
+    const int rows = min(BM, a.M - m0);
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(a.A + (long)m0 * a.lda), (short)0,
+                                             rows * a.lda * 2, RSRC_W3);
 #pragma unroll
-  for (int p = 0; p < PER; ++p) {
-    const int r = (lane >> 3) + 8 * wm + 32 * p;
-    int gr;
-    if (grp == 0) {
-      gr = m0 + r;
-      ok[p] = gr < a.M;
-      src[p] = a.A + (long)(ok[p] ? gr : 0) * a.lda + kc * 8;
-    } else {
-      gr = epi.template w_row<BN, TN>(tn, r);
-      ok[p] = gr >= 0;
-      src[p] = a.W + (long)(ok[p] ? gr : 0) * a.ldw + kc * 8;
+    for (int p = 0; p < PER; ++p) {
+      const int r = (lane >> 3) + 8 * wm + 32 * p;
+      voff[p] = r < rows ? (uint32_t)(r * a.lda + kc * 8) * 2u : kNoRow;
+    }
+  } else {
+    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(a.W), (short)0, a.w_bytes, RSRC_W3);
+#pragma unroll
+    for (int p = 0; p < PER; ++p) {
+      const int r = (lane >> 3) + 8 * wm + 32 * p;
+      const int gr = epi.template w_row<BN, TN>(tn, r);
+      voff[p] = gr >= 0 ? (uint32_t)(gr * a.ldw + kc * 8) * 2u : kNoRow;
     }
   }
   bf16* const dst0 = grp == 0 ? &sA[0][0] : &sB[0][0];
   u32x4 stage[PER];
-  const u32x4 zero4 = {0u, 0u, 0u, 0u};
-  auto fetch = [&](int k0) __attribute__((always_inline)) {
+  auto fetch = [&](int k0, int h) __attribute__((always_inline)) {
 #pragma unroll
-    for (int p = 0; p < PER; ++p) stage[p] = *reinterpret_cast<const u32x4*>(src[p] + k0);
+    for (int p = h * HPER; p < (h + 1) * HPER; ++p)
+      stage[p] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff[p], k0 * 2, 0);
   };
-  auto stash = [&](int buf) __attribute__((always_inline)) {
+  auto stash = [&](int buf, int h) __attribute__((always_inline)) {
     bf16* dst = dst0 + buf * (BM * BK);
 #pragma unroll
-    for (int p = 0; p < PER; ++p) {
+    for (int p = h * HPER; p < (h + 1) * HPER; ++p) {
       const int r = (lane >> 3) + 8 * wm + 32 * p;
-      *reinterpret_cast<u32x4*>(&dst[swz(r, kc)]) = ok[p] ? stage[p] : zero4;
+      *reinterpret_cast<u32x4*>(&dst[swz(r, kc)]) = stage[p];
     }
   };
 
@@ -411,9 +296,6 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
     for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
 
   bf16x8 fa[2][FM], fb[2][FN];
-  auto init_acc = [&]() __attribute__((always_inline)) {
-    if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
-  };
   auto read_frags = [&](int cur, int h) __attribute__((always_inline)) {
 #pragma unroll
     for (int k2 = 0; k2 < 2; ++k2) {
@@ -444,27 +326,32 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
   };
 
   const int ksteps = a.K / BK;
-  fetch(0);
-  init_acc();  // its loads overlap the first tile's
-  stash(0);
-  if (ksteps > 1) fetch(BK);
+  // prologue: K step 0 in LDS, K step 1 in the stage registers
+  fetch(0, 0);
+  fetch(0, 1);
+  if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
+  stash(0, 0);
+  stash(0, 1);
+  if (ksteps > 1) {
+    fetch(BK, 0);
+    fetch(BK, 1);
+  }
   phase();
   if (grp == 1) phase();  // group 1 runs one phase behind
 
   for (int ks = 0; ks < ksteps; ++ks) {
     const int cur = ks & 1;
-    read_frags(cur, 0);
-    phase();
-    mma();
-    phase();
-    read_frags(cur, 1);
-    if (ks + 1 < ksteps) {
-      stash(cur ^ 1);
-      if (ks + 2 < ksteps) fetch((ks + 2) * BK);
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      read_frags(cur, h);
+      if (ks + 1 < ksteps) {
+        stash(cur ^ 1, h);
+        if (ks + 2 < ksteps) fetch((ks + 2) * BK, h);
+      }
+      phase();
+      mma();
+      phase();
     }
-    phase();
-    mma();
-    phase();
   }
   if (grp == 0) phase();  // match group 1's extra barrier
 
@@ -476,9 +363,14 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
 constexpr int kBM = 256, kBN = 256, kWM = 4, kWN = 2;
 
 template <class Epi>
-hipError_t launch(const GemmArgs& a, const Epi& epi, hipStream_t s) {
+hipError_t launch(GemmArgs a, const Epi& epi, hipStream_t s) {
   const int tiles = cdiv(a.M, 256) * epi.tiles_n(256);
   if (tiles == 0) return hipSuccess;
+  // operand offsets are 32-bit buffer offsets: W and a 256-row A panel must
+  // stay below 2 GiB, and K must be whole 64-wide steps
+  const long w_bytes = (long)epi.w_rows() * a.ldw * 2, a_panel = 256L * a.lda * 2;
+  if (w_bytes >= (1L << 31) || a_panel >= (1L << 31) || a.K % BK) return hipErrorInvalidValue;
+  a.w_bytes = (int)w_bytes;
   hipLaunchKernelGGL((gemm_pp_kernel<Epi>), dim3(tiles), dim3(512), 0, s, a, epi);
   return hipGetLastError();
 }
@@ -487,14 +379,14 @@ hipError_t launch(const GemmArgs& a, const Epi& epi, hipStream_t s) {
 
 hipError_t gemm_residual(const void* A, int lda, const void* W, int ldw, int M, int N, int K,
                          float* R, int ldr, hipStream_t s) {
-  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K};
+  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K, 0};
   EpiResidual e{R, ldr, N};
   return launch(a, e, s);
 }
 
 hipError_t gemm_swiglu(const void* A, int lda, const void* W, int ldw, int M, int F, int K,
                        void* act, hipStream_t s) {
-  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K};
+  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K, 0};
   EpiSwiGLU e{(bf16*)act, F};
   return launch(a, e, s);
 }
@@ -502,7 +394,7 @@ hipError_t gemm_swiglu(const void* A, int lda, const void* W, int ldw, int M, in
 hipError_t gemm_qkv_rope(const void* A, int lda, const void* W, int ldw, int M, int K, int Hq,
                          int Hkv, int dh, int n_seq, int pos0, const float* cos_t,
                          const float* sin_t, const QkvOut& o, hipStream_t s) {
-  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K};
+  GemmArgs a{(const bf16*)A, lda, (const bf16*)W, ldw, M, K, 0};
   if (dh == 128) {
     EpiQKV<128> e{(bf16*)o.q, (bf16*)o.k, (bf16*)o.v, o.q_sb, o.q_sh, o.k_sb, o.k_sh,
                   o.v_sb, o.v_sh, Hq, Hkv, n_seq, pos0, cos_t, sin_t, (const bf16*)o.bias};
