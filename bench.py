@@ -81,8 +81,8 @@ def main():
     ap.add_argument("--depth-steps", type=int, default=3, help="timed steps per extra depth")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--profile-step", action="store_true",
-                    help="run one warm step at --depth plus a 512 MiB copy (counter calibration) and exit; "
-                         "the command profiled under rocprofv3")
+                    help="run the warmup and timed steps at --depth plus a 512 MiB copy (counter calibration) "
+                         "and exit; the command profiled under rocprofv3")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -115,8 +115,9 @@ def main():
     out = torch.empty((B, n_s, cfg["hidden"]), dtype=torch.float32, device=dev)
 
     if args.profile_step:
-        model.step(key, xs, d, out=out)
-        model.step(key, xs, d, out=out)
+        # the bench's warmup and timed steps, back to back, for the profiler
+        for _ in range(args.warmup + args.steps):
+            model.step(key, xs, d, out=out)
         # plain copy of known size: 512 MiB read + 512 MiB written, the
         # reference that scales the HBM byte counters
         src = torch.empty(256 * 2 ** 20, dtype=torch.float16, device=dev).fill_(1.0)
