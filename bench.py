@@ -395,8 +395,7 @@ def cpu_baseline(cfg, B, m, n_s, d, log, n_req=6):
     except Exception:
         threads = os.cpu_count()
     log("bench: timing the fp64 oracle sample on the host")
-    w = [{k: synth.to_f64(v) for k, v in synth.layer_weights(cfg, l, 3000, device="cuda").items()}
-         for l in (0, 1)]
+    w = synth.weights_f64([synth.layer_weights(cfg, l, 3000, device="cuda") for l in (0, 1)])
     xp, xs = synth.step_inputs(cfg, B, m, n_s, 3500, device="cuda")
     xp, xs = synth.to_f64(xp), synth.to_f64(xs[:n_req])
     torch.cuda.empty_cache()

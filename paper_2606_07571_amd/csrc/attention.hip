@@ -26,15 +26,17 @@
 // (no data movement; the MFMA's k order is chosen to match the keys a lane
 // already holds) and V^T is read from a transposed LDS copy of the V tile.
 // Softmax runs in fp32 in the log2 domain (exp2 with log2(e) folded into the
-// scale); P is rounded to bf16 for the P.V product and the row sum adds the
-// fp32 probabilities.
+// scale); P is rounded to bf16 for the P.V product, and the row sums are taken
+// on the matrix pipe from the same bf16 probabilities (one 16x16x32 MFMA per
+// 16 keys against a 0/1 selector), so the weights that multiply V are the
+// ones that are normalised and no vector adds are spent on the sums.
 //
 // Software pipeline.  Every wave overlaps its own matrix and vector work: in
 // step u it runs
 //   block A: O^T += V(u-1)^T . P(u-1)^T (16 MFMAs) alongside the softmax of
 //            S(u) (row max, running max, P(u) = exp2(...), row sums)
 //   block B: S(u+1)^T = K(u+1) . Q^T (16 MFMAs) alongside this thread's share
-//            of the LDS fill of tile u+2 and the global fetch of tile u+3
+//            of the LDS fill of tile u+2 and the global fetch of tile u+4
 // and one barrier.  The MFMAs of a block do not depend on its vector work, so
 // the two streams issue side by side, and with two such waves per SIMD the
 // vector instructions issue at the SIMD's full rate (one wave alone issues
@@ -44,8 +46,11 @@
 // done, is rescaled between the blocks.
 //
 // LDS.  Tiles live in a 4-deep ring (tile t in slot t % 4): step u reads
-// V(u-1) and K(u+1) and fills tile u+2, whose slot last held tile u-2.  Rows
-// are padded by 16 bytes (K rows dh+8 elements, V^T rows 72), so the 16 rows
+// V(u-1) and K(u+1) and fills tile u+2, whose slot last held tile u-2.  The
+// global fetch of a tile lands in one of two register staging sets (tile t in
+// set t % 2) two steps before its LDS fill, so a fetch that misses the L2 has
+// two steps to arrive.
+// Rows are padded by 16 bytes (K rows dh+8 elements, V^T rows 72), so the 16 rows
 // that one fragment read touches fall into distinct bank groups and every
 // fragment of a tile sits at a compile-time offset from one per-lane base.
 // In a V^T row the 16 keys of k step s are stored in the order
@@ -162,7 +167,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   enter(0, b_lo);
   // valid keys of each fetched tile for this wave (0 for tiles of another
   // request and past the end), queued from fetch to use: tiles u..u+3
-  int nvq0 = 0, nvq1 = 0, nvq2 = 0, nvq3 = 0;
+  int nvq0 = 0, nvq1 = 0, nvq2 = 0, nvq3 = 0, nvq4 = 0;
 
   // this thread's share of a fill: K chunks q = tid + 512p (row q / KCH,
   // chunk q % KCH); V key pair kp = tid % 32 of dim group tid / 32
@@ -182,13 +187,14 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   const int vpos = ((2 * (kp >> 3) + ((kp >> 1) & 1)) << 3) + ((kp >> 2) & 1) * 4 + 2 * (kp & 1);
   const int vs_off = KTILE + dg * 8 * VROW + vpos;
 
-  u32x4 kreg[K_PER], vreg[2];
+  u32x4 kreg[2][K_PER], vreg[2][2];   // two staging sets: tile t in set t % 2
   // fetch of the tile at the cursor, which then moves on; tiles past the end
   // get an empty descriptor, so their loads return zeros
-  auto fetch = [&]() __attribute__((always_inline)) {
+  auto fetch = [&](auto set_c) __attribute__((always_inline)) {
+    constexpr int S = decltype(set_c)::value;
     const int nv = min(KT, w_left);
     const int bytes = nv * DH * 2;
-    nvq3 = (active && (w_req < 0 || w_req == b)) ? nv : 0;
+    nvq4 = (active && (w_req < 0 || w_req == b)) ? nv : 0;
     const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wk), (short)0, bytes, RSRC_W3);
     const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wv), (short)0, bytes, RSRC_W3);
     if (w_left > KT) {
@@ -201,18 +207,19 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       else enter(own_pre ? 1 : 2, w_req + 1);
     }
 #pragma unroll
-    for (int p = 0; p < K_PER; ++p) kreg[p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
-    vreg[0] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off, 0, 0);
-    vreg[1] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off + DH * 2, 0, 0);
+    for (int p = 0; p < K_PER; ++p) kreg[S][p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
+    vreg[S][0] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off, 0, 0);
+    vreg[S][1] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off + DH * 2, 0, 0);
   };
-  auto stash = [&](int slot) __attribute__((always_inline)) {
+  auto stash = [&](int slot, auto set_c) __attribute__((always_inline)) {
+    constexpr int S = decltype(set_c)::value;
     bf16* base = smem + slot * SLOT;
 #pragma unroll
-    for (int p = 0; p < K_PER; ++p) *reinterpret_cast<u32x4*>(base + ks_off[p]) = kreg[p];
+    for (int p = 0; p < K_PER; ++p) *reinterpret_cast<u32x4*>(base + ks_off[p]) = kreg[S][p];
     if (v_ok) {
 #pragma unroll
       for (int e = 0; e < 8; ++e) {
-        const uint32_t w = __builtin_amdgcn_perm(vreg[1][e >> 1], vreg[0][e >> 1], (e & 1) ? 0x07060302u : 0x05040100u);
+        const uint32_t w = __builtin_amdgcn_perm(vreg[S][1][e >> 1], vreg[S][0][e >> 1], (e & 1) ? 0x07060302u : 0x05040100u);
         *reinterpret_cast<uint32_t*>(base + vs_off + e * VROW) = w;
       }
     }
@@ -222,7 +229,18 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
 #pragma unroll
   for (int nb = 0; nb < NB; ++nb) o[nb] = zero16();
   // running row max m (log2 units) and row sum l
-  float m_run = -1e30f, l_run = 0.f;
+  float m_run = -1e30f;
+  // Row sums on the matrix pipe: D(16x16) = A . P^T with A rows 0 and 1
+  // selecting the lanes that hold query rows c and c + 16 (lanes 0, 32 and
+  // 17, 49 supply ones), so lanes 0..15 accumulate the sums of rows l and
+  // l + 16 of the bf16 probabilities in elements 0 and 1.
+  f32x4 lacc = {0.f, 0.f, 0.f, 0.f};
+  bf16x8 ones_sel;
+  {
+    const uint32_t w1 = (lane == 0 || lane == 32 || lane == 17 || lane == 49) ? 0x3f803f80u : 0u;
+    const u32x4 v = {w1, w1, w1, w1};
+    ones_sel = __builtin_bit_cast(bf16x8, v);
+  }
   const float sl2 = a.scale * 1.4426950408889634f;
   const int k_rd = c * KROW + half * 8;                // lane's K fragment base
   const int v_rd = KTILE + c * VROW + half * 8;        // lane's V^T fragment base
@@ -261,16 +279,14 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       }
   };
   // P^T operand of k step s: slot (half, e) is key 16s + 8(e/4) + 4half +
-  // e%4, i.e. score element 8(s%2) + e of block s/2; lt accumulates the fp32
-  // probabilities (four partial sums)
-  auto probs = [&](const f32x16 (&sc)[2], int s, float (&lt)[4]) __attribute__((always_inline)) {
+  // e%4, i.e. score element 8(s%2) + e of block s/2
+  auto probs = [&](const f32x16 (&sc)[2], int s) __attribute__((always_inline)) {
     uint32_t pw[4];
 #pragma unroll
     for (int w = 0; w < 4; ++w) {
       const int e0 = 8 * (s & 1) + 2 * w;
       const float p0 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][e0], sl2, -m_run));
       const float p1 = __builtin_amdgcn_exp2f(fmaf(sc[s >> 1][e0 + 1], sl2, -m_run));
-      lt[w] += p0 + p1;
       pw[w] = pack_bf16x2(p0, p1);
     }
     const u32x4 pv4 = {pw[0], pw[1], pw[2], pw[3]};
@@ -330,10 +346,10 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
         f[i] = *reinterpret_cast<const bf16x8*>(kt + (i & 1) * 32 * KROW + (kk0 + (i >> 1)) * 16);
     }
   };
-  auto step = [&](int u, auto has_pv, bf16x8 (&p)[NS], f32x16 (&sc)[2], bf16x8 (&fr)[2][4])
+  auto step = [&](int u, auto has_pv, auto set_c, bf16x8 (&p)[NS], f32x16 (&sc)[2], bf16x8 (&fr)[2][4])
       __attribute__((always_inline)) {
     constexpr bool PV = decltype(has_pv)::value;
-    float lt[4] = {0.f, 0.f, 0.f, 0.f};
+    f32x4 ltile = {0.f, 0.f, 0.f, 0.f};
     const int nv = nvq0;
     if (nv < KT) mask(sc, nv);
     if constexpr (!PV) load_sub(NS, u, fr[NS & 1]);
@@ -350,10 +366,11 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
           for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(fr[j & 1][nb], p[j], o[nb]);
         }
         if (j == 0) alpha = new_max(sc);
-        p[j] = probs(sc, j, lt);
+        p[j] = probs(sc, j);
         // pin P(u)'s step j here: otherwise the compiler defers the softmax
         // past the QK MFMAs and keeps a second copy of S(u) alive
         asm volatile("" : "+v"(p[j]));
+        ltile = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_sel, p[j], ltile, 0, 0, 0);
       } else {
         const int kk0 = 2 * (j - NS);
 #pragma unroll
@@ -361,8 +378,8 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
           const int kk = kk0 + (i >> 1), kb = i & 1;
           sc[kb] = mfma_32x32x16(fr[j & 1][i], qf[kk], kk == 0 ? zero16() : sc[kb]);
         }
-        if (j == NS) stash((u + 2) % NBUF);
-        if (j == NS + 1 || (NQS == 1 && j == NS)) fetch();   // tile u+3
+        if (j == NS) stash((u + 2) % NBUF, set_c);              // tile u+2, fetched two steps ago
+        if (j == NS + 1 || (NQS == 1 && j == NS)) fetch(set_c);   // tile u+4
       }
       // reads first, then MFMAs each followed by a share of the VALU work
       if (PV || j >= NS) {
@@ -372,6 +389,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
           __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
           __builtin_amdgcn_sched_group_barrier(0x002, 10, 0);
         }
+        if (j < NS) __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);
       }
       __builtin_amdgcn_sched_barrier(0);
       if (j == NS - 1) {
@@ -381,8 +399,11 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
           for (int nb = 0; nb < NB; ++nb)
 #pragma unroll
             for (int e = 0; e < 16; ++e) o[nb][e] *= alpha;
+          lacc[0] *= alpha;
+          lacc[1] *= __shfl(alpha, (lane & 15) + 16, 64);
         }
-        l_run = fmaf(l_run, alpha, (lt[0] + lt[1]) + (lt[2] + lt[3]));
+        lacc[0] += ltile[0];
+        lacc[1] += ltile[1];
       }
     }
     // keep each step's work on its own side of the barrier
@@ -392,31 +413,42 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     nvq0 = nvq1;
     nvq1 = nvq2;
     nvq2 = nvq3;
+    nvq3 = nvq4;
   };
   using T_ = std::true_type;
   using F_ = std::false_type;
 
   // prologue: tiles 0 and 1 in LDS, tile 2 in flight, S(0) computed
-  fetch();
-  nvq0 = nvq3;
-  stash(0);
-  fetch();
-  nvq1 = nvq3;
-  stash(1);
-  fetch();
-  nvq2 = nvq3;
+  using S0 = std::integral_constant<int, 0>;
+  using S1 = std::integral_constant<int, 1>;
+  fetch(S0{});
+  nvq0 = nvq4;
+  fetch(S1{});
+  nvq1 = nvq4;
+  stash(0, S0{});
+  stash(1, S1{});
+  fetch(S0{});
+  nvq2 = nvq4;
+  fetch(S1{});
+  nvq3 = nvq4;
   __syncthreads();
   bf16x8 p[NS];
   f32x16 sc[2];
   bf16x8 fr[2][4];
   qk(0, sc);
   // (the last step's S(n_tiles) reads a zero-filled slot and is discarded)
-  step(0, F_{}, p, sc, fr);
-  for (int u = 1; u < n_tiles; ++u) step(u, T_{}, p, sc, fr);
+  step(0, F_{}, S0{}, p, sc, fr);
+  int u = 1;
+  for (; u + 1 < n_tiles; u += 2) {
+    step(u, T_{}, S1{}, p, sc, fr);
+    step(u + 1, T_{}, S0{}, p, sc, fr);
+  }
+  if (u < n_tiles) step(u, T_{}, S1{}, p, sc, fr);
   pv(n_tiles - 1, p);
 
+  const float l0 = __shfl(lacc[0], c & 15, 64), l1 = __shfl(lacc[1], c & 15, 64);
   if (!row_ok) return;
-  const float inv = 1.f / half_sum(l_run);
+  const float inv = 1.f / (c < 16 ? l0 : l1);
   if constexpr (OUT_F32) {
     float* op = (float*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
 #pragma unroll
