@@ -100,6 +100,33 @@ def main():
     torch.cuda.set_device(dev)
     log = lambda *a: print(*a, file=sys.stderr, flush=True)
 
+    # ---------------------------------------------------------------- attention configs
+    # Measured first, on their own inputs, before the long full-step runs heat
+    # the card: 5 warm-up launches, then the median of 3 repetitions of 20.
+    attention = {}
+    for cid in (() if args.profile_step else (0, 1, 2, 4)):
+        s = synth.ATTN_CONFIGS[cid]
+        ins = synth.attention_inputs(s, 1000 * cid, device=dev)
+        o = torch.empty((s.B, s.Hq, s.n_s, s.dh), dtype=torch.float32, device=dev)
+        for _ in range(5):
+            bc.shared_prefix_attention(*ins, out=o)
+        torch.cuda.synchronize()
+        n, reps = 20, []
+        for _ in range(3):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            for _ in range(n):
+                bc.shared_prefix_attention(*ins, out=o)
+            e1.record()
+            torch.cuda.synchronize()
+            reps.append(e0.elapsed_time(e1) / n)
+        t = sorted(reps)[1]
+        fl = 4.0 * s.B * s.Hq * s.n_s * (s.m + s.n_s) * s.dh
+        attention[f"C{cid}"] = {"ms": round(t, 4), "tflops": round(fl / (t / 1e3) / 1e12, 1),
+                                "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
+        del ins, o
+    torch.cuda.empty_cache()
+
     # ---------------------------------------------------------------- C3 setup
     cfg = synth.model_config()
     sc = synth.STEP_CONFIG
@@ -288,28 +315,6 @@ def main():
     model.close()
     del weights, model
     torch.cuda.empty_cache()
-
-    # ---------------------------------------------------------------- attention configs
-    attention = {}
-    for cid in (0, 1, 2, 4):
-        s = synth.ATTN_CONFIGS[cid]
-        ins = synth.attention_inputs(s, 1000 * cid, device=dev)
-        o = torch.empty((s.B, s.Hq, s.n_s, s.dh), dtype=torch.float32, device=dev)
-        for _ in range(3):
-            bc.shared_prefix_attention(*ins, out=o)
-        torch.cuda.synchronize()
-        n = 20
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        for _ in range(n):
-            bc.shared_prefix_attention(*ins, out=o)
-        e1.record()
-        torch.cuda.synchronize()
-        t = e0.elapsed_time(e1) / n
-        fl = 4.0 * s.B * s.Hq * s.n_s * (s.m + s.n_s) * s.dh
-        attention[f"C{cid}"] = {"ms": round(t, 4), "tflops": round(fl / (t / 1e3) / 1e12, 1),
-                                "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
-        del ins, o
 
     # ---------------------------------------------------------------- Dream-7B-shaped full step
     # 28 layers, GQA 28/4 x 128, hidden 3584, SwiGLU 18944, Q/K/V bias; the GQA
