@@ -253,7 +253,8 @@ def main():
 
     # ------------------------------------------------ profiling (Eq. 3, Sec. 5.1)
     # sim_{l,1} of the 16 requests at every layer: the un-cached step storing
-    # every layer's K/V, then the HBM-bound similarity reduction per layer
+    # every layer's K/V, then the HBM-bound similarity reduction (one call
+    # covers every layer)
     sims = model.profile_similarity(key, xs)
     torch.cuda.synchronize()
     t_prof = timed(lambda: model.profile_similarity(key, xs, sims=sims), args.depth_steps)
@@ -264,7 +265,7 @@ def main():
     kv_layer_bytes = 2 * Hkv * m * dh * 2
     sim_bytes = L * (kv_layer_bytes + B * kv_layer_bytes)   # KV$ once, each request's KV^ref once
     profiling = {"requests": B, "layers": L, "profile_ms": round(t_prof, 3),
-                 "similarity_ms": round(sim_ms, 4), "similarity_launch_pairs": sim_n,
+                 "similarity_ms": round(sim_ms, 4), "similarity_calls": sim_n,
                  "similarity_bytes": sim_bytes,
                  "similarity_gbs": round(sim_bytes / (sim_ms / 1e3) / 1e9, 1),
                  "similarity_frac_of_hbm": round(sim_bytes / (sim_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),

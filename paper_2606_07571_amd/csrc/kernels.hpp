@@ -58,22 +58,24 @@ struct AttnArgs {
 };
 hipError_t attention(const AttnArgs& a, hipStream_t s);
 
-// ----- KV similarity (Eq. 3): out[b * out_stride] = cos(flatten(a), flatten(r_b))
-// for b < B.  Both sides are P parts x H heads x E contiguous elements (E a
-// multiple of 8): cached element (p, g, i) at a + p*a_part + g*a_head + i,
-// request b's at r + p*r_part + b*r_req + g*r_head + i (bf16).  `partial` is
-// scratch of kv_cosine_partial_bytes(v) bytes; out is fp64.
+// ----- KV similarity (Eq. 3): out[b * out_req + l * out_layer] =
+// cos(flatten(a_l), flatten(r_{l,b})) for b < B, l < L.  Both sides are L
+// layers x P parts x H heads x E contiguous elements (E a multiple of 8):
+// cached element (l, p, g, i) at a + l*a_layer + p*a_part + g*a_head + i,
+// request b's at r + l*r_layer + p*r_part + b*r_req + g*r_head + i (bf16).
+// `partial` is scratch of kv_cosine_partial_bytes(v) bytes; out is fp64.
 struct CosView {
   const void* a;
-  long a_part, a_head;
+  long a_layer, a_part, a_head;
   const void* r;
-  long r_part, r_req, r_head;
-  int P, H;
+  long r_layer, r_part, r_req, r_head;
+  int L, P, H;
   long E;
   int B;
 };
 size_t kv_cosine_partial_bytes(const CosView& v);
-hipError_t kv_cosine(const CosView& v, double* partial, double* out, long out_stride, hipStream_t s);
+hipError_t kv_cosine(const CosView& v, double* partial, double* out, long out_req, long out_layer,
+                     hipStream_t s);
 
 // ----- elementwise / normalisation
 // out[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gain)

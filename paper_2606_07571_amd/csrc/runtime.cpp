@@ -524,6 +524,7 @@ struct ProfilePlan {
 
 bc::CosView kv_view(const bc_model_config& c, int m, int B) {
   bc::CosView v{};
+  v.L = c.n_layers;
   v.P = 2;
   v.H = c.n_kv_heads;
   v.E = (long)m * c.head_dim;
@@ -823,24 +824,26 @@ bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suf
   const EntryLayout e = entry_layout(c, m, L);
   const DeepLayout dl = deep_layout(c, m, B, n_s, 0);
   const char* cm = (const char*)ent->mem;
-  for (int l = 0; l < L; ++l) {
-    bc::CosView v = kv_view(c, m, B);
-    v.a = cm + (size_t)(2 * l) * e.kv_layer;   // KV$_l: K then V, [Hkv][m][dh] each
-    v.a_part = (long)(e.kv_layer / 2);
-    v.a_head = (long)m * c.head_dim;
-    v.r = ws + pp.store + (size_t)(2 * l) * dl.part;  // request b's prefix rows of layer l
-    v.r_part = (long)(dl.part / 2);
-    v.r_req = dl.sb;
-    v.r_head = dl.sh;
-    BC_LAUNCH(model, BC_K_KVSIM, s, bc::kv_cosine(v, (double*)(ws + pp.partial), sims + l, L, s));
-  }
+  // every layer in one reduction: layer l's KV$ (K then V, [Hkv][m][dh] each)
+  // against each request's prefix rows of layer l in the store
+  bc::CosView v = kv_view(c, m, B);
+  v.a = cm;
+  v.a_layer = (long)e.kv_layer;   // elements: 2 blocks of kv_layer bytes
+  v.a_part = (long)(e.kv_layer / 2);
+  v.a_head = (long)m * c.head_dim;
+  v.r = ws + pp.store;
+  v.r_layer = (long)dl.part;
+  v.r_part = (long)(dl.part / 2);
+  v.r_req = dl.sb;
+  v.r_head = dl.sh;
+  BC_LAUNCH(model, BC_K_KVSIM, s, bc::kv_cosine(v, (double*)(ws + pp.partial), sims, L, 1, s));
   return ok();
 }
 
 size_t bc_cosine_workspace_bytes(long n) {
   if (n <= 0 || n % 8) return 0;
   bc::CosView v{};
-  v.P = v.H = v.B = 1;
+  v.L = v.P = v.H = v.B = 1;
   v.E = n;
   return bc::kv_cosine_partial_bytes(v);
 }
@@ -855,9 +858,9 @@ bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out
   bc::CosView v{};
   v.a = a;
   v.r = b;
-  v.P = v.H = v.B = 1;
+  v.L = v.P = v.H = v.B = 1;
   v.E = n;
-  BC_HIP(bc::kv_cosine(v, (double*)workspace, out, 1, (hipStream_t)stream));
+  BC_HIP(bc::kv_cosine(v, (double*)workspace, out, 1, 1, (hipStream_t)stream));
   return ok();
 }
 
