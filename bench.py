@@ -83,6 +83,9 @@ def main():
     ap.add_argument("--profile-step", action="store_true",
                     help="run the warmup and timed steps at --depth plus a 512 MiB copy (counter calibration) "
                          "and exit; the command profiled under rocprofv3")
+    ap.add_argument("--profile-attention", action="store_true",
+                    help="run the attention configurations (5 warm-up and 5 more launches each) and exit; "
+                         "the command profiled under rocprofv3")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -108,9 +111,13 @@ def main():
         s = synth.ATTN_CONFIGS[cid]
         ins = synth.attention_inputs(s, 1000 * cid, device=dev)
         o = torch.empty((s.B, s.Hq, s.n_s, s.dh), dtype=torch.float32, device=dev)
-        for _ in range(5):
+        for _ in range(10 if args.profile_attention else 5):
             bc.shared_prefix_attention(*ins, out=o)
         torch.cuda.synchronize()
+        if args.profile_attention:
+            log(f"profiled C{cid}: 10 launches")
+            del ins, o
+            continue
         n, reps = 20, []
         for _ in range(3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -126,6 +133,8 @@ def main():
                                 "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4)}
         del ins, o
     torch.cuda.empty_cache()
+    if args.profile_attention:
+        return
 
     # ---------------------------------------------------------------- C3 setup
     cfg = synth.model_config()
@@ -194,7 +203,24 @@ def main():
     # per-kernel breakdown of one extra profiled step (all classes)
     model.profile_begin()
     model.step(key, xs, d, out=out)
-    breakdown = {k: round(v[0], 3) for k, v in model.profile_end().items()}
+    prof = model.profile_end()
+    breakdown = {k: round(v[0], 3) for k, v in prof.items()}
+    # HBM-bound paths of the same step against the 8 TB/s peak, algorithmic
+    # bytes only: RMSNorm reads the fp32 residual and writes the bf16 operand
+    # (two norms per layer over B*n_s rows below d, B*(m+n_s) rows from d on);
+    # the transition writes the full residual of every request and reads the
+    # suffix rows and the cached prefix residual once
+    h = cfg["hidden"]
+    norm_rows = 2 * (d * B * n_s + (L - d) * B * (m + n_s))
+    norm_bytes = norm_rows * h * (4 + 2)
+    trans_bytes = (B * (m + n_s) + B * n_s + m) * h * 4 if d < L else 0
+    hbm = {}
+    for name, nbytes in (("rmsnorm", norm_bytes), ("transition", trans_bytes)):
+        if name in prof and nbytes:
+            t_ms = prof[name][0]
+            hbm[name] = {"ms": round(t_ms, 3), "launches": prof[name][1], "bytes": nbytes,
+                         "gbs": round(nbytes / (t_ms / 1e3) / 1e9, 1),
+                         "frac": round(nbytes / (t_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4)}
 
     # ---------------------------------------------------------------- other depths
     per_depth = {}
@@ -270,6 +296,8 @@ def main():
                  "similarity_gbs": round(sim_bytes / (sim_ms / 1e3) / 1e9, 1),
                  "similarity_frac_of_hbm": round(sim_bytes / (sim_ms / 1e3) / 1e9 / PEAK_HBM_GBS, 4),
                  "sim_layer_mean_min": [round(float(x), 6) for x in (sims.mean().item(), sims.min().item())]}
+    hbm["kv_similarity"] = {"ms": profiling["similarity_ms"], "launches": sim_n, "bytes": sim_bytes,
+                            "gbs": profiling["similarity_gbs"], "frac": profiling["similarity_frac_of_hbm"]}
     del sims
     torch.cuda.empty_cache()
 
@@ -378,6 +406,7 @@ def main():
         "multi_prefix": multi_prefix,
         "profiling": profiling,
         "kernel_ms_one_step": breakdown,
+        "hbm": hbm,
         "attention": attention,
         "dream_step": dream,
         "populate_ms": {"m1536_L32": round(populate_ms, 2), "m8192_L8": round(pop4_ms, 2)},

@@ -361,9 +361,11 @@ enum {
   BC_K_OPROJ = 4,       /* output projection + residual add */
   BC_K_GATE_UP = 5,     /* gate/up projection + SwiGLU */
   BC_K_DOWN = 6,        /* down projection + residual add */
-  BC_K_OTHER = 7,       /* RoPE table, input widening, transition, suffix gather */
+  BC_K_OTHER = 7,       /* RoPE table, input widening, suffix gather */
   BC_K_KVSIM = 8,       /* KV-similarity reduction of bc_profile_similarity */
-  BC_K_COUNT = 9
+  BC_K_TRANSITION = 9,  /* full residual at l = d: cached prefix residual broadcast to
+                           every request, followed by its suffix rows */
+  BC_K_COUNT = 10
 };
 
 /* Starts timing, with HIP events recorded on the launch stream around every

@@ -88,7 +88,7 @@ _SIGS = {
 
 # kernel classes of bc_profile_* (include/bicache.h)
 KERNEL_CLASSES = ("rmsnorm", "qkv_rope", "attn_shared", "attn_full", "o_proj", "gate_up_swiglu",
-                  "down", "other", "kv_similarity")
+                  "down", "other", "kv_similarity", "transition")
 
 _lib = None
 

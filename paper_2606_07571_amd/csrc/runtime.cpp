@@ -426,7 +426,7 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
       const int m = ents[g]->m, cnt = groups[g].count;
       const EntryLayout e = entry_layout(c, m, ents[g]->n_layers);
       const float* hdp = (const float*)((const char*)ents[g]->mem + e.h_off + (size_t)d * e.h_layer);
-      BC_LAUNCH(model, BC_K_OTHER, s,
+      BC_LAUNCH(model, BC_K_TRANSITION, s,
                 bc::build_full_residual(hdp, out + first * n_s * h, R + row0 * h, cnt, m, n_s, h, s));
       row0 += (long)cnt * (m + n_s);
       first += cnt;
