@@ -33,6 +33,17 @@ def test_library_exports_every_declared_symbol():
         assert hasattr(L, s), f"{s} not exported"
 
 
+def test_kernel_classes_match_header_enum():
+    # the binding names the timing classes of bc_profile_begin/end in enum order
+    text = open(HEADER).read()
+    enum = dict((k, int(v)) for k, v in re.findall(r"\b(BC_K_[A-Z_]+)\s*=\s*(\d+)", text))
+    assert enum.pop("BC_K_COUNT") == len(_lib.KERNEL_CLASSES)
+    assert sorted(enum.values()) == list(range(len(_lib.KERNEL_CLASSES)))
+    assert _lib.KERNEL_CLASSES[enum["BC_K_TRANSITION"]] == "transition"
+    assert _lib.KERNEL_CLASSES[enum["BC_K_KVSIM"]] == "kv_similarity"
+    assert _lib.KERNEL_CLASSES[enum["BC_K_RMSNORM"]] == "rmsnorm"
+
+
 def test_prefix_key_matches_xxhash_and_oracle():
     rng = np.random.default_rng(0)
     for n in (0, 1, 7, 8, 9, 31, 32, 33, 1536, 8192):
