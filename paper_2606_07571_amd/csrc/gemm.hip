@@ -242,7 +242,14 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
 
   const int tiles_m = cdiv(a.M, BM), tiles_n = epi.tiles_n(BN);
   const int lid = xcd_remap(blockIdx.x, gridDim.x);
-  constexpr int GM = 8;
+  // Tile order: each die takes a contiguous range of tiles, swept in groups
+  // of GM row tiles, column-major inside a group, so the 32 tiles a die runs
+  // at once share A and W panels in its L2.  When a row of tiles is at most
+  // 32 wide (the O and down projections: N = h), whole rows run at once
+  // (GM = 1): every A panel is then read from HBM once and the small W is
+  // re-read from the last-level cache (measured +2% and +4% on the O and down
+  // shapes against GM = 8, which suits the wide QKV and gate/up outputs).
+  const int GM = tiles_n <= 32 ? 1 : 8;
   const int per_group = GM * tiles_n;
   const int first_m = (lid / per_group) * GM;
   const int gsz = min(tiles_m - first_m, GM);
