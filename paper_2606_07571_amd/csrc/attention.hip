@@ -24,7 +24,8 @@
 // none until the end.  The output is accumulated transposed as well,
 // O^T += V^T . P^T: the P^T operand comes straight from the score registers
 // (no data movement; the MFMA's k order is chosen to match the keys a lane
-// already holds) and V^T is read from a transposed LDS copy of the V tile.
+// already holds) and the V^T operand is read from the row-major V tile with
+// transposing LDS reads (ds_read_b64_tr_b16).
 // Softmax runs in fp32 in the log2 domain (exp2 with log2(e) folded into the
 // scale); P is rounded to bf16 for the P.V product, and the row sums are taken
 // on the matrix pipe from the same bf16 probabilities (one 16x16x32 MFMA per
@@ -50,12 +51,17 @@
 // global fetch of a tile lands in one of two register staging sets (tile t in
 // set t % 2) two steps before its LDS fill, so a fetch that misses the L2 has
 // two steps to arrive.
-// Rows are padded by 16 bytes (K rows dh+8 elements, V^T rows 72), so the 16 rows
-// that one fragment read touches fall into distinct bank groups and every
-// fragment of a tile sits at a compile-time offset from one per-lane base.
-// In a V^T row the 16 keys of k step s are stored in the order
-// [0-3, 8-11, 4-7, 12-15], which makes the 8 keys lane half h of the P.V MFMA
-// takes (16s + 4h + {0..3} and 16s + 8 + 4h + {0..3}) one 16-byte chunk.
+// K and V tiles are both stored as they are in memory, one key per row, filled
+// with 16-byte writes.  K rows are padded by 16 bytes (dh+8 elements), so the
+// 16 rows that one K fragment read touches fall into distinct bank groups; V
+// rows by 64 bytes (dh+32), so the 4 rows x 32 bytes of each 16-lane group of
+// a transposing read, and both groups of a half wave, hit distinct banks.
+// Every fragment of a tile sits at a compile-time offset from one per-lane
+// base.  A V^T fragment (8 keys of one dim per lane) is two transposing reads:
+// keys 16s + 4h + {0..3} and 16s + 8 + 4h + {0..3} for lane half h, the order
+// of the P^T operand's k slots.  (An earlier V^T copy transposed in registers
+// before the fill measured the same on the large shapes and 2-8% slower on
+// short walks.)
 // Global fetches are buffer loads whose descriptor covers exactly the tile's
 // valid rows, so key rows past the end of a partial tile (and whole tiles past
 // the end of the sequence) read as zero with no masking code.  Key rows of
@@ -77,8 +83,8 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   constexpr int NW = 8, QR = 32;
   constexpr int KCH = DH / 8;                  // 16-byte chunks per key row
   constexpr int KROW = DH + 8;                 // K row stride in LDS (elements)
-  constexpr int VROW = KT + 8;                 // V^T row stride in LDS (elements)
-  constexpr int KTILE = KT * KROW, VTILE = DH * VROW, SLOT = KTILE + VTILE;
+  constexpr int VROW = DH + 32;                // V row stride in LDS (elements): rows 16 banks apart
+  constexpr int KTILE = KT * KROW, VTILE = KT * VROW, SLOT = KTILE + VTILE;
   constexpr int NBUF = 4;
   constexpr int K_PER = KT * KCH / 512;        // 16-byte K chunks per thread per tile
   constexpr int NB = DH / 32, NKK = DH / 16, NS = KT / 16;
@@ -169,8 +175,8 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   // request and past the end), queued from fetch to use: tiles u..u+3
   int nvq0 = 0, nvq1 = 0, nvq2 = 0, nvq3 = 0, nvq4 = 0;
 
-  // this thread's share of a fill: K chunks q = tid + 512p (row q / KCH,
-  // chunk q % KCH); V key pair kp = tid % 32 of dim group tid / 32
+  // this thread's share of a fill: K and V chunks q = tid + 512p (row q / KCH,
+  // chunk q % KCH)
   int kg_off[K_PER], ks_off[K_PER];
 #pragma unroll
   for (int p = 0; p < K_PER; ++p) {
@@ -178,16 +184,14 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     kg_off[p] = (r * DH + kc * 8) * 2;                 // bytes from the tile's first row
     ks_off[p] = r * KROW + kc * 8;                     // elements in the LDS K tile
   }
-  const int kp = tid & 31, dgl = tid >> 5;
-  const bool v_ok = KCH * 32 >= 512 || dgl < KCH;   // always, for dh 128
-  const int dg = v_ok ? dgl : 0;
-  const int vg_off = (2 * kp * DH + dg * 8) * 2;
-  // key 2kp sits at position chunk*8 + elem of its V^T row, with the 16 keys
-  // of step s stored in the order [0-3, 8-11, 4-7, 12-15]
-  const int vpos = ((2 * (kp >> 3) + ((kp >> 1) & 1)) << 3) + ((kp >> 2) & 1) * 4 + 2 * (kp & 1);
-  const int vs_off = KTILE + dg * 8 * VROW + vpos;
+  int vs_off[K_PER];
+#pragma unroll
+  for (int p = 0; p < K_PER; ++p) {
+    const int q = tid + 512 * p, r = q / KCH, kc = q % KCH;
+    vs_off[p] = KTILE + r * VROW + kc * 8;             // elements in the LDS slot
+  }
 
-  u32x4 kreg[2][K_PER], vreg[2][2];   // two staging sets: tile t in set t % 2
+  u32x4 kreg[2][K_PER], vreg[2][K_PER];   // two staging sets: tile t in set t % 2
   // fetch of the tile at the cursor, which then moves on; tiles past the end
   // get an empty descriptor, so their loads return zeros
   auto fetch = [&](auto set_c) __attribute__((always_inline)) {
@@ -208,21 +212,16 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     }
 #pragma unroll
     for (int p = 0; p < K_PER; ++p) kreg[S][p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
-    vreg[S][0] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off, 0, 0);
-    vreg[S][1] = __builtin_amdgcn_raw_buffer_load_b128(rv, vg_off + DH * 2, 0, 0);
+#pragma unroll
+    for (int p = 0; p < K_PER; ++p) vreg[S][p] = __builtin_amdgcn_raw_buffer_load_b128(rv, kg_off[p], 0, 0);
   };
   auto stash = [&](int slot, auto set_c) __attribute__((always_inline)) {
     constexpr int S = decltype(set_c)::value;
     bf16* base = smem + slot * SLOT;
 #pragma unroll
     for (int p = 0; p < K_PER; ++p) *reinterpret_cast<u32x4*>(base + ks_off[p]) = kreg[S][p];
-    if (v_ok) {
 #pragma unroll
-      for (int e = 0; e < 8; ++e) {
-        const uint32_t w = __builtin_amdgcn_perm(vreg[S][1][e >> 1], vreg[S][0][e >> 1], (e & 1) ? 0x07060302u : 0x05040100u);
-        *reinterpret_cast<uint32_t*>(base + vs_off + e * VROW) = w;
-      }
-    }
+    for (int p = 0; p < K_PER; ++p) *reinterpret_cast<u32x4*>(base + vs_off[p]) = vreg[S][p];
   };
 
   f32x16 o[NB];
@@ -243,17 +242,29 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   }
   const float sl2 = a.scale * 1.4426950408889634f;
   const int k_rd = c * KROW + half * 8;                // lane's K fragment base
-  const int v_rd = KTILE + c * VROW + half * 8;        // lane's V^T fragment base
+  // V^T fragment (dims nb*32 + c, the 8 keys of k slots (half, 0..7) of k
+  // step s) from two transposed reads of the row-major V tile: in each group
+  // of 16 lanes (G = lane / 16, j = lane % 16) lane j addresses dims
+  // 16(G%2) + 4(j%4) .. +3 of key row 4(G/2) + j/4 (+ 16s, + 8 for the keys of
+  // slots 4..7), and lane i of the group receives dim i of the 4 rows
+  // addressed by lanes 4k + i/4, k = 0..3.
+  const int v_rd = KTILE + (4 * (lane >> 5) + ((lane & 15) >> 2)) * VROW + 16 * ((lane >> 4) & 1) + 4 * (lane & 3);
 
+  auto vfrag = [&](const bf16* vt, int nb, int s) __attribute__((always_inline)) {
+    typedef short s16x4 __attribute__((ext_vector_type(4)));
+    const s16x4 lo = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(vt + 16 * s * VROW + nb * 32));
+    const s16x4 hi = __builtin_amdgcn_ds_read_tr16_b64_v4i16(
+        (__attribute__((address_space(3))) s16x4*)(vt + (16 * s + 8) * VROW + nb * 32));
+    const s16x4 w[2] = {lo, hi};
+    return __builtin_bit_cast(bf16x8, w);
+  };
   auto pv = [&](int t, const bf16x8 (&p)[NS]) __attribute__((always_inline)) {
     const bf16* vt = smem + (t % NBUF) * SLOT + v_rd;
 #pragma unroll
     for (int s = 0; s < NS; ++s)
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) {
-        const bf16x8 vf = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + s * 16);
-        o[nb] = mfma_32x32x16(vf, p[s], o[nb]);
-      }
+      for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(vfrag(vt, nb, s), p[s], o[nb]);
   };
   auto qk = [&](int t, f32x16 (&sc)[2]) __attribute__((always_inline)) {
     const bf16* kt = smem + (t % NBUF) * SLOT + k_rd;
@@ -337,7 +348,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     if (j < NS) {
       const bf16* vt = smem + ((u + NBUF - 1) % NBUF) * SLOT + v_rd;
 #pragma unroll
-      for (int nb = 0; nb < NB; ++nb) f[nb] = *reinterpret_cast<const bf16x8*>(vt + nb * 32 * VROW + j * 16);
+      for (int nb = 0; nb < NB; ++nb) f[nb] = vfrag(vt, nb, j);
     } else {
       const bf16* kt = smem + ((u + 1) % NBUF) * SLOT + k_rd;
       const int kk0 = 2 * (j - NS);
