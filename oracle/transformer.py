@@ -34,6 +34,8 @@ is taken to be the prefix-only residual cached by populate.  A consequence
 that the tests check: the prefix K/V recomputed at layer d equal the cached
 KV$_d exactly.
 """
+import os
+
 import numpy as np
 
 from .attention import attention, kv_head_of
@@ -105,20 +107,43 @@ def project_qkv(x_res, lw, cfg, positions):
     return q, k, v
 
 
+def _workers():
+    """Host threads the oracle may use (OMP_NUM_THREADS when set)."""
+    try:
+        n = int(os.environ.get("OMP_NUM_THREADS", "0"))
+    except ValueError:
+        n = 0
+    return max(1, n or (os.cpu_count() or 1))
+
+
 def attend(q, k_all, v_all, cfg):
     """Attention of every query head over the given K/V (no mask, Eq. 2).
 
     q: [Hq, n_q, dh]; k_all, v_all: [Hkv, n_k, dh].  Returns the attention
     output laid out token-major [n_q, Hq*dh] (head h occupies columns
     h*dh .. h*dh+dh-1), which is the input of the output projection.
+
+    Heads are independent (each is Eq. 2 on its own Q/K/V), so large ones run
+    on a pool of host threads, one head per task with single-threaded BLAS;
+    every head's arithmetic is the same as in a serial loop.
     """
     Hq, n_q, dh = q.shape
     Hkv = k_all.shape[0]
     scale = 1.0 / np.sqrt(dh)
-    o = np.empty((Hq, n_q, dh), dtype=np.float64)
-    for h in range(Hq):
+
+    def one_head(h):
         g = kv_head_of(h, Hq, Hkv)
-        o[h] = attention(q[h], k_all[g], v_all[g], scale)
+        return attention(q[h], k_all[g], v_all[g], scale)
+
+    workers = min(Hq, _workers())
+    if workers > 1 and n_q * k_all.shape[1] >= (1 << 20):
+        from concurrent.futures import ThreadPoolExecutor
+        from threadpoolctl import threadpool_limits
+        with threadpool_limits(limits=1, user_api="blas"), ThreadPoolExecutor(workers) as ex:
+            heads = list(ex.map(one_head, range(Hq)))
+    else:
+        heads = [one_head(h) for h in range(Hq)]
+    o = np.stack(heads)
     return o.transpose(1, 0, 2).reshape(n_q, Hq * dh)
 
 

@@ -73,7 +73,7 @@ def _compile(src):
 def build_host_lib():
     os.makedirs(os.path.dirname(HOST_LIB), exist_ok=True)
     cxx = shutil.which("g++") or "c++"
-    cmd = [cxx, "-O2", "-std=c++17", "-shared", "-fPIC", f"-I{CSRC}",
+    cmd = [cxx, "-O2", "-std=c++17", "-shared", "-fPIC", "-Wl,-Bsymbolic", f"-I{CSRC}",
            os.path.join(ROOT, "tests", "native", "table_shim.cpp"),
            os.path.join(CSRC, "xxh64.cpp"), "-o", HOST_LIB]
     subprocess.run(cmd, check=True)

@@ -31,20 +31,24 @@ class CacheTable {
   }
   bool contains(uint64_t key) const { return map_.count(key) != 0; }
 
-  // Inserts a key that is not present.  When the table is full the oldest
-  // entry is evicted first; returns true and sets *evicted_key in that case.
+  // Inserts a key that is not present.  When the table was full the oldest
+  // entry is evicted; returns true and sets *evicted_key in that case.  Every
+  // allocation happens before anything is removed, so a failed one
+  // (std::bad_alloc) leaves the table exactly as it was.
   bool insert(uint64_t key, const CacheEntry& e, uint64_t* evicted_key) {
-    bool ev = false;
-    if ((int)map_.size() >= capacity_) {
-      const uint64_t old = order_.front();
-      order_.pop_front();
-      map_.erase(old);
-      *evicted_key = old;
-      ev = true;
+    auto it = map_.emplace(key, e).first;
+    try {
+      order_.push_back(key);
+    } catch (...) {
+      map_.erase(it);
+      throw;
     }
-    map_.emplace(key, e);
-    order_.push_back(key);
-    return ev;
+    if ((int)map_.size() <= capacity_) return false;
+    const uint64_t old = order_.front();
+    order_.pop_front();
+    map_.erase(old);
+    *evicted_key = old;
+    return true;
   }
 
   bool erase(uint64_t key) {

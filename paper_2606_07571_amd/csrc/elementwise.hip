@@ -69,21 +69,23 @@ __global__ void bf16_to_f32_kernel(const bf16* __restrict__ in, float* __restric
   reinterpret_cast<f32x4*>(out)[2 * i + 1] = b;
 }
 
-// grid.y = request b, grid.x covers the N*h/4 float4 of one request.
+// One lane per float4 of R [B][N][h]: request b = i / (N*h/4), element
+// i % (N*h/4) of its rows (a 1-D grid, so B has no grid-dimension limit).
 __global__ void build_full_kernel(const f32x4* __restrict__ pre, const f32x4* __restrict__ suf,
-                                  f32x4* __restrict__ R, long pre4, long suf4) {
+                                  f32x4* __restrict__ R, long pre4, long suf4, long total4) {
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  const long b = blockIdx.y;
-  if (i >= pre4 + suf4) return;
-  R[b * (pre4 + suf4) + i] = i < pre4 ? pre[i] : suf[b * suf4 + (i - pre4)];
+  if (i >= total4) return;
+  const long b = i / (pre4 + suf4), j = i - b * (pre4 + suf4);
+  R[i] = j < pre4 ? pre[j] : suf[b * suf4 + (j - pre4)];
 }
 
+// One lane per float4 of out [B][n_s][h].
 __global__ void gather_suffix_kernel(const f32x4* __restrict__ R, f32x4* __restrict__ out,
-                                     long pre4, long suf4) {
+                                     long pre4, long suf4, long total4) {
   const long i = (long)blockIdx.x * blockDim.x + threadIdx.x;
-  const long b = blockIdx.y;
-  if (i >= suf4) return;
-  out[b * suf4 + i] = R[b * (pre4 + suf4) + pre4 + i];
+  if (i >= total4) return;
+  const long b = i / suf4, j = i - b * suf4;
+  out[i] = R[b * (pre4 + suf4) + pre4 + j];
 }
 
 // Angles in double: pos * theta^(-2i/dh) reaches ~1e4 rad, where an fp32
@@ -129,17 +131,17 @@ hipError_t bf16_to_f32(const void* in, float* out, long n, hipStream_t s) {
 
 hipError_t build_full_residual(const float* pre, const float* suf, float* R, int B, int m,
                                int n_s, int h, hipStream_t s) {
-  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4;
-  hipLaunchKernelGGL(build_full_kernel, dim3((unsigned)((pre4 + suf4 + 255) / 256), B), dim3(256),
-                     0, s, (const f32x4*)pre, (const f32x4*)suf, (f32x4*)R, pre4, suf4);
+  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4, total4 = (long)B * (pre4 + suf4);
+  hipLaunchKernelGGL(build_full_kernel, dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0, s,
+                     (const f32x4*)pre, (const f32x4*)suf, (f32x4*)R, pre4, suf4, total4);
   return hipGetLastError();
 }
 
 hipError_t gather_suffix(const float* R, float* out, int B, int m, int n_s, int h,
                          hipStream_t s) {
-  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4;
-  hipLaunchKernelGGL(gather_suffix_kernel, dim3((unsigned)((suf4 + 255) / 256), B), dim3(256), 0,
-                     s, (const f32x4*)R, (f32x4*)out, pre4, suf4);
+  const long pre4 = (long)m * h / 4, suf4 = (long)n_s * h / 4, total4 = (long)B * suf4;
+  hipLaunchKernelGGL(gather_suffix_kernel, dim3((unsigned)((total4 + 255) / 256)), dim3(256), 0,
+                     s, (const f32x4*)R, (f32x4*)out, pre4, suf4, total4);
   return hipGetLastError();
 }
 

@@ -15,7 +15,9 @@
 #include <cstdint>
 #include <new>
 #include <string>
+#include <mutex>
 #include <unordered_map>
+#include <unordered_set>
 #include <vector>
 
 #include "../../include/bicache.h"
@@ -56,24 +58,51 @@ struct bc_model {
 
 namespace {
 
-thread_local std::string g_err;
+// The calling thread's last error message; a fixed buffer, so that reporting
+// a failed host allocation needs no allocation itself.
+thread_local char g_err[512];
 
 bc_status fail(bc_status st, const char* fmt, ...) {
-  char buf[512];
   va_list ap;
   va_start(ap, fmt);
-  vsnprintf(buf, sizeof buf, fmt, ap);
+  vsnprintf(g_err, sizeof g_err, fmt, ap);
   va_end(ap);
-  g_err = buf;
   return st;
 }
 
 bc_status ok() {
-  g_err.clear();
+  g_err[0] = 0;
   return BC_OK;
 }
 
+// Status of a C++ exception caught at the boundary (none crosses it): a failed
+// host allocation is BC_E_OOM, anything else BC_E_INVALID.
+bc_status host_exception() {
+  try {
+    throw;
+  } catch (const std::bad_alloc&) {
+    return fail(BC_E_OOM, "host allocation failed");
+  } catch (const std::exception& e) {
+    return fail(BC_E_INVALID, "host error: %s", e.what());
+  } catch (...) {
+    return fail(BC_E_INVALID, "unknown host error");
+  }
+}
+
+// Handles of the models that exist: a call with a destroyed or unknown handle
+// is refused (BC_E_INVALID) instead of reading freed memory.
+std::mutex g_models_mu;
+std::unordered_set<const bc_model*> g_models;
+
+bool live(const bc_model* m) {
+  if (!m) return false;
+  std::lock_guard<std::mutex> lk(g_models_mu);
+  return g_models.count(m) != 0;
+}
+
 constexpr size_t kAlign = 256;
+constexpr uintptr_t kVecAlign = 16;  // kernels move 16-byte vectors
+bool misaligned(const void* p) { return ((uintptr_t)p % kVecAlign) != 0; }
 constexpr int kMaxGroups = 4096;  // prefix groups in one batch
 size_t align_up(size_t x) { return (x + kAlign - 1) / kAlign * kAlign; }
 
@@ -302,7 +331,8 @@ bool step_shape_ok(const bc_model_config& c, int m, int B, int n_s, int d, std::
   const long N = (long)m + n_s;
   const long rows = (long)B * N;
   const long widest = c.ffn > (long)c.n_heads * c.head_dim ? c.ffn : (long)c.n_heads * c.head_dim;
-  if (N > INT_MAX / 2 || rows > INT_MAX / 2 || rows * (widest > c.hidden ? widest : c.hidden) > (1L << 40)) {
+  if (N > INT_MAX / 2 || rows > INT_MAX / 2 || rows * (widest > c.hidden ? widest : c.hidden) > (1L << 40) ||
+      rows * (long)c.hidden / 4 > (long)INT_MAX) {
     snprintf(buf, sizeof buf, "step too large (B=%d, m+n_s=%ld)", B, N);
     *why = buf;
     return false;
@@ -330,7 +360,8 @@ struct Group {
 bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const void* x_suffix,
                     int n_s, int d, int mode, void* store, size_t store_bytes, float* out,
                     void* workspace, size_t ws_bytes, void* stream) {
-  if (!model || !groups || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (!live(model) || !groups || !x_suffix || !out || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (misaligned(x_suffix) || misaligned(out)) return fail(BC_E_INVALID, "x_suffix and out must be 16-byte aligned");
   if (mode != BC_DEEP_REFRESH && mode != BC_DEEP_REUSE) return fail(BC_E_INVALID, "unknown deep mode %d", mode);
   if (n_groups < 1 || n_groups > kMaxGroups)
     return fail(BC_E_INVALID, "n_groups=%d outside [1, %d]", n_groups, kMaxGroups);
@@ -353,7 +384,8 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
     full_rows += (long)groups[g].count * (m + n_s);
     if (m + n_s > max_N) max_N = m + n_s;
   }
-  if (B > INT_MAX / 2 || full_rows > INT_MAX / 2 || full_rows * (long)c.hidden > (1L << 40))
+  // the elementwise kernels run one lane per 4 residual values on a 1-D grid
+  if (B > INT_MAX / 2 || full_rows > INT_MAX / 2 || full_rows * (long)c.hidden / 4 > (long)INT_MAX)
     return fail(BC_E_INVALID, "step too large (B=%ld, %ld full rows)", B, full_rows);
   const bool full = mode == BC_DEEP_REFRESH && d < L;  // deep layers run over all rows
   const long rows_max = full ? full_rows : B * n_s;
@@ -381,6 +413,10 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
                   "deep store was refreshed for key %016llx m=%d B=%d n_s=%d d=%d, not key %016llx m=%d B=%ld n_s=%d d=%d",
                   (unsigned long long)tg.key, tg.m, tg.B, tg.n_s, tg.d, (unsigned long long)key0, m0, B, n_s, d);
   }
+
+  // A refresh overwrites the store: its old tag no longer describes it, even if
+  // a launch below fails part way.  The new tag is set once every launch is in.
+  if (use_store && mode == BC_DEEP_REFRESH) model->deep_tags.erase((uintptr_t)store);
 
   hipStream_t s = (hipStream_t)stream;
   char* ws = (char*)workspace;
@@ -481,6 +517,9 @@ bc_status prefix_attention(const void* q, const void* k_pre, const void* v_pre, 
                            int Hkv, int m, int n_s, int dh, float scale, void* stream) {
   if (!q || !k_suf || !v_suf || !out || (m > 0 && (!k_pre || !v_pre)))
     return fail(BC_E_INVALID, "null argument");
+  if (misaligned(q) || misaligned(k_suf) || misaligned(v_suf) || misaligned(out) ||
+      (m > 0 && (misaligned(k_pre) || misaligned(v_pre))))
+    return fail(BC_E_INVALID, "q, k, v and out must be 16-byte aligned");
   if (B < 1 || n_s < 1 || m < 0) return fail(BC_E_INVALID, "B, n_s >= 1 and m >= 0 required");
   if (dh != 64 && dh != 128) return fail(BC_E_INVALID, "dh must be 64 or 128 (got %d)", dh);
   if (Hq < 1 || Hkv < 1 || Hq % Hkv) return fail(BC_E_INVALID, "Hq must be a positive multiple of Hkv");
@@ -550,10 +589,10 @@ ProfilePlan profile_plan(const bc_model* model, int m, int B, int n_s) {
 
 extern "C" {
 
-const char* bc_last_error(void) { return g_err.c_str(); }
+const char* bc_last_error(void) { return g_err; }
 
 bc_status bc_model_create(const bc_model_config* cfg, const bc_layer_weights* layers,
-                          int cache_capacity, bc_model** out) {
+                          int cache_capacity, bc_model** out) try {
   if (!cfg || !layers || !out) return fail(BC_E_INVALID, "null argument");
   std::string why;
   if (!config_ok(*cfg, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
@@ -562,28 +601,47 @@ bc_status bc_model_create(const bc_model_config* cfg, const bc_layer_weights* la
     const bc_layer_weights& w = layers[l];
     if (!w.w_qkv || !w.w_o || !w.w_gate_up || !w.w_down || !w.attn_norm || !w.ffn_norm)
       return fail(BC_E_INVALID, "layer %d has a null weight pointer", l);
+    if (misaligned(w.w_qkv) || misaligned(w.w_o) || misaligned(w.w_gate_up) || misaligned(w.w_down) ||
+        misaligned(w.attn_norm) || misaligned(w.ffn_norm) || misaligned(w.b_qkv))
+      return fail(BC_E_INVALID, "layer %d has a weight pointer that is not 16-byte aligned", l);
   }
   bc_model* m = new (std::nothrow) bc_model(*cfg, layers, cache_capacity);
   if (!m) return fail(BC_E_OOM, "host allocation of the model failed");
+  try {
+    std::lock_guard<std::mutex> lk(g_models_mu);
+    g_models.insert(m);
+  } catch (...) {
+    delete m;
+    throw;
+  }
   *out = m;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-bc_status bc_model_destroy(bc_model* model) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_model_destroy(bc_model* model) try {
+  {
+    std::lock_guard<std::mutex> lk(g_models_mu);
+    if (!model || g_models.erase(model) == 0) return fail(BC_E_INVALID, "null, unknown or destroyed model");
+  }
   delete model;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-size_t bc_prefix_cache_bytes(const bc_model* model, int m, int n_layers_to_cache) {
-  if (!model || m < 1 || n_layers_to_cache < 0 || n_layers_to_cache > model->cfg.n_layers) return 0;
+size_t bc_prefix_cache_bytes(const bc_model* model, int m, int n_layers_to_cache) try {
+  if (!live(model) || m < 1 || n_layers_to_cache < 0 || n_layers_to_cache > model->cfg.n_layers) return 0;
   return entry_layout(model->cfg, m, n_layers_to_cache).total;
+} catch (...) {
+  return 0;
 }
 
 size_t bc_cache_offset(const bc_model* model, int m, int Lc, int layer, int part, int head,
-                       int pos, int dim) {
+                       int pos, int dim) try {
   const size_t bad = (size_t)-1;
-  if (!model || m < 1 || Lc < 0 || Lc > model->cfg.n_layers) return bad;
+  if (!live(model) || m < 1 || Lc < 0 || Lc > model->cfg.n_layers) return bad;
   const bc_model_config& c = model->cfg;
   const EntryLayout e = entry_layout(c, m, Lc);
   if (pos < 0 || pos >= m || dim < 0) return bad;
@@ -597,20 +655,25 @@ size_t bc_cache_offset(const bc_model* model, int m, int Lc, int layer, int part
     return e.h_off + (size_t)layer * e.h_layer + ((size_t)pos * c.hidden + dim) * 4;
   }
   return bad;
+} catch (...) {
+  return 0;
 }
 
-size_t bc_populate_workspace_bytes(const bc_model* model, int m) {
-  if (!model || m < 1) return 0;
+size_t bc_populate_workspace_bytes(const bc_model* model, int m) try {
+  if (!live(model) || m < 1) return 0;
   return make_plan(model->cfg, m, m, false, m).total;
+} catch (...) {
+  return 0;
 }
 
 bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix, int m,
                              int n_layers_to_cache, void* cache_mem, size_t cache_bytes,
                              void* workspace, size_t ws_bytes, void* stream,
-                             uint64_t* evicted_key, int* evicted) {
+                             uint64_t* evicted_key, int* evicted) try {
   if (evicted) *evicted = 0;
   if (evicted_key) *evicted_key = 0;
-  if (!model || !x_prefix || !cache_mem || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (!live(model) || !x_prefix || !cache_mem || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (misaligned(x_prefix)) return fail(BC_E_INVALID, "x_prefix must be 16-byte aligned");
   const bc_model_config& c = model->cfg;
   const int Lc = n_layers_to_cache;
   if (m < 1) return fail(BC_E_INVALID, "prefix length m=%d must be >= 1", m);
@@ -656,25 +719,31 @@ bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix
     if (evicted_key) *evicted_key = ev;
   }
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-bc_status bc_prefix_lookup(const bc_model* model, uint64_t key, int* m_out, int* n_layers_out) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_prefix_lookup(const bc_model* model, uint64_t key, int* m_out, int* n_layers_out) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   const bc::CacheEntry* e = model->table.find(key);
   if (!e) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
   if (m_out) *m_out = e->m;
   if (n_layers_out) *n_layers_out = e->n_layers;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-bc_status bc_prefix_invalidate(bc_model* model, uint64_t key) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_prefix_invalidate(bc_model* model, uint64_t key) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   if (!model->table.erase(key)) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-bc_status bc_cache_keys(const bc_model* model, uint64_t* keys, int max_keys, int* n_out) {
-  if (!model || !n_out || max_keys < 0 || (max_keys > 0 && !keys)) return fail(BC_E_INVALID, "bad argument");
+bc_status bc_cache_keys(const bc_model* model, uint64_t* keys, int max_keys, int* n_out) try {
+  if (!live(model) || !n_out || max_keys < 0 || (max_keys > 0 && !keys)) return fail(BC_E_INVALID, "bad argument");
   int i = 0;
   for (uint64_t k : model->table.order()) {
     if (i < max_keys) keys[i] = k;
@@ -682,9 +751,11 @@ bc_status bc_cache_keys(const bc_model* model, uint64_t* keys, int max_keys, int
   }
   *n_out = i;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-uint64_t bc_prefix_key(const int32_t* token_ids, size_t n) {
+uint64_t bc_prefix_key(const int32_t* token_ids, size_t n) try {
   // little-endian int32 bytes, independent of the host's byte order
   std::vector<unsigned char> bytes(n * 4);
   for (size_t i = 0; i < n; ++i) {
@@ -692,16 +763,20 @@ uint64_t bc_prefix_key(const int32_t* token_ids, size_t n) {
     for (int b = 0; b < 4; ++b) bytes[i * 4 + b] = (unsigned char)(v >> (8 * b));
   }
   return bc::xxh64(bytes.data(), bytes.size(), 0);
+} catch (...) {
+  return 0;
 }
 
-size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int d) {
-  if (!model) return 0;
+size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int d) try {
+  if (!live(model)) return 0;
   return step_workspace(model, &m, &B, 1, n_s, d);
+} catch (...) {
+  return 0;
 }
 
 size_t bc_step_multi_workspace_bytes(const bc_model* model, const uint64_t* keys, const int* counts,
-                                     int n_groups, int n_s, int d) {
-  if (!model || !keys || !counts || n_groups < 1 || n_groups > kMaxGroups) return 0;
+                                     int n_groups, int n_s, int d) try {
+  if (!live(model) || !keys || !counts || n_groups < 1 || n_groups > kMaxGroups) return 0;
   std::vector<int> ms(n_groups);
   for (int g = 0; g < n_groups; ++g) {
     const bc::CacheEntry* e = model->table.find(keys[g]);
@@ -709,11 +784,13 @@ size_t bc_step_multi_workspace_bytes(const bc_model* model, const uint64_t* keys
     ms[g] = e->m;
   }
   return step_workspace(model, ms.data(), counts, n_groups, n_s, d);
+} catch (...) {
+  return 0;
 }
 
 bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int* rows,
-                       int* pos_base, int* reads_kv, int* reads_h) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+                       int* pos_base, int* reads_kv, int* reads_h) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   std::string why;
   if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
   const int L = model->cfg.n_layers;
@@ -725,27 +802,33 @@ bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int*
   }
   if (reads_h) *reads_h = d < L ? d : -1;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
 
 bc_status bc_step_forward(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
-                          int d, float* out, void* workspace, size_t ws_bytes, void* stream) {
+                          int d, float* out, void* workspace, size_t ws_bytes, void* stream) try {
   const Group g{key, B};
   return step_impl(model, &g, 1, x_suffix, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out, workspace,
                    ws_bytes, stream);
+} catch (...) {
+  return host_exception();
 }
 
-size_t bc_deep_store_bytes(const bc_model* model, int m, int B, int n_s, int d) {
-  if (!model) return 0;
+size_t bc_deep_store_bytes(const bc_model* model, int m, int B, int n_s, int d) try {
+  if (!live(model)) return 0;
   std::string why;
   if (!step_shape_ok(model->cfg, m, B, n_s, d, &why)) return 0;
   return deep_layout(model->cfg, m, B, n_s, d).total;
+} catch (...) {
+  return 0;
 }
 
 size_t bc_deep_store_offset(const bc_model* model, int m, int B, int n_s, int d, int layer,
-                            int part, int req, int head, int pos, int dim) {
+                            int part, int req, int head, int pos, int dim) try {
   const size_t bad = (size_t)-1;
-  if (!model) return bad;
+  if (!live(model)) return bad;
   const bc_model_config& c = model->cfg;
   std::string why;
   if (!step_shape_ok(c, m, B, n_s, d, &why)) return bad;
@@ -755,30 +838,38 @@ size_t bc_deep_store_offset(const bc_model* model, int m, int B, int n_s, int d,
   const DeepLayout dl = deep_layout(c, m, B, n_s, d);
   return (size_t)(2 * (layer - d) + part) * dl.part +
          ((size_t)req * dl.sb + (size_t)head * dl.sh + (size_t)pos * c.head_dim + dim) * 2;
+} catch (...) {
+  return 0;
 }
 
-bc_status bc_deep_store_reset(bc_model* model, const void* deep_store) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_deep_store_reset(bc_model* model, const void* deep_store) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   model->deep_tags.erase((uintptr_t)deep_store);
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-int bc_is_refresh_step(int t, int delta) {
+int bc_is_refresh_step(int t, int delta) try {
   if (t < 1 || delta < 1) return -1;
   return (t - 1) % delta == 0 ? 1 : 0;
+} catch (...) {
+  return -1;
 }
 
 bc_status bc_step_forward_deep(bc_model* model, uint64_t key, const void* x_suffix, int B,
                                int n_s, int d, int mode, void* deep_store, size_t store_bytes,
-                               float* out, void* workspace, size_t ws_bytes, void* stream) {
+                               float* out, void* workspace, size_t ws_bytes, void* stream) try {
   const Group g{key, B};
   return step_impl(model, &g, 1, x_suffix, n_s, d, mode, deep_store, store_bytes, out, workspace,
                    ws_bytes, stream);
+} catch (...) {
+  return host_exception();
 }
 
 bc_status bc_step_forward_multi(bc_model* model, const uint64_t* keys, const int* counts,
                                 int n_groups, const void* x_suffix, int n_s, int d, float* out,
-                                void* workspace, size_t ws_bytes, void* stream) {
+                                void* workspace, size_t ws_bytes, void* stream) try {
   if (!keys || !counts) return fail(BC_E_INVALID, "null argument");
   if (n_groups < 1 || n_groups > kMaxGroups)
     return fail(BC_E_INVALID, "n_groups=%d outside [1, %d]", n_groups, kMaxGroups);
@@ -786,19 +877,24 @@ bc_status bc_step_forward_multi(bc_model* model, const uint64_t* keys, const int
   for (int g = 0; g < n_groups; ++g) gs[g] = Group{keys[g], counts[g]};
   return step_impl(model, gs.data(), n_groups, x_suffix, n_s, d, BC_DEEP_REFRESH, nullptr, 0, out,
                    workspace, ws_bytes, stream);
+} catch (...) {
+  return host_exception();
 }
 
 // ------------------------------------------------------- shared-prefix profiling
 
 
-size_t bc_profile_workspace_bytes(const bc_model* model, int m, int B, int n_s) {
-  if (!model) return 0;
+size_t bc_profile_workspace_bytes(const bc_model* model, int m, int B, int n_s) try {
+  if (!live(model)) return 0;
   return profile_plan(model, m, B, n_s).total;
+} catch (...) {
+  return 0;
 }
 
 bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suffix, int B, int n_s,
-                                double* sims, void* workspace, size_t ws_bytes, void* stream) {
-  if (!model || !x_suffix || !sims || !workspace) return fail(BC_E_INVALID, "null argument");
+                                double* sims, void* workspace, size_t ws_bytes, void* stream) try {
+  if (!live(model) || !x_suffix || !sims || !workspace) return fail(BC_E_INVALID, "null argument");
+  if (misaligned(x_suffix) || misaligned(sims)) return fail(BC_E_INVALID, "x_suffix and sims must be 16-byte aligned");
   const bc::CacheEntry* ent = model->table.find(key);
   if (!ent) return fail(BC_E_NOT_FOUND, "key %016llx is not cached", (unsigned long long)key);
   const bc_model_config& c = model->cfg;
@@ -807,6 +903,8 @@ bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suf
     return fail(BC_E_INVALID, "profiling needs KV$ of all %d layers; the entry caches %d", L, ent->n_layers);
   std::string why;
   if (!step_shape_ok(c, m, B, n_s, 0, &why)) return fail(BC_E_INVALID, "%s", why.c_str());
+  if ((long)L * 2 * c.n_kv_heads > 65535)
+    return fail(BC_E_CAPACITY, "similarity reduction supports at most 65535 (layer, K/V, head) blocks");
   const ProfilePlan pp = profile_plan(model, m, B, n_s);
   if (!pp.total) return fail(BC_E_INVALID, "invalid profiling shape");
   if (ws_bytes < pp.total) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, pp.total);
@@ -838,21 +936,25 @@ bc_status bc_profile_similarity(bc_model* model, uint64_t key, const void* x_suf
   v.r_head = dl.sh;
   BC_LAUNCH(model, BC_K_KVSIM, s, bc::kv_cosine(v, (double*)(ws + pp.partial), sims, L, 1, s));
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-size_t bc_cosine_workspace_bytes(long n) {
+size_t bc_cosine_workspace_bytes(long n) try {
   if (n <= 0 || n % 8) return 0;
   bc::CosView v{};
   v.L = v.P = v.H = v.B = 1;
   v.E = n;
   return bc::kv_cosine_partial_bytes(v);
+} catch (...) {
+  return 0;
 }
 
 bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out, void* workspace,
-                               size_t ws_bytes, void* stream) {
+                               size_t ws_bytes, void* stream) try {
   if (!a || !b || !out || !workspace) return fail(BC_E_INVALID, "null argument");
   if (n <= 0 || n % 8) return fail(BC_E_INVALID, "n=%ld must be a positive multiple of 8", n);
-  if ((uintptr_t)a % 16 || (uintptr_t)b % 16) return fail(BC_E_INVALID, "operands must be 16-byte aligned");
+  if (misaligned(a) || misaligned(b) || misaligned(out)) return fail(BC_E_INVALID, "a, b and out must be 16-byte aligned");
   const size_t need = bc_cosine_workspace_bytes(n);
   if (ws_bytes < need) return fail(BC_E_INVALID, "workspace %zu < required %zu", ws_bytes, need);
   bc::CosView v{};
@@ -862,17 +964,21 @@ bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out
   v.E = n;
   BC_HIP(bc::kv_cosine(v, (double*)workspace, out, 1, 1, (hipStream_t)stream));
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-int bc_shallow_depth(const double* sims, int n_layers, double tau) {
+int bc_shallow_depth(const double* sims, int n_layers, double tau) try {
   if (!sims || n_layers < 0) return -1;
   int b = 0;
   while (b < n_layers && sims[b] >= tau) ++b;
   return b;
+} catch (...) {
+  return -1;
 }
 
 bc_status bc_build_depth_table(const double* ratios, const int* depths, int n, int n_buckets,
-                               int* table) {
+                               int* table) try {
   if (!ratios || !depths || !table || n < 0 || n_buckets < 1) return fail(BC_E_INVALID, "bad argument");
   std::vector<long> sum(n_buckets + 1, 0), cnt(n_buckets + 1, 0);
   for (int i = 0; i < n; ++i) {
@@ -887,27 +993,33 @@ bc_status bc_build_depth_table(const double* ratios, const int* depths, int n, i
   table[0] = -1;
   for (int k = 1; k <= n_buckets; ++k) table[k] = cnt[k] ? (int)(sum[k] / cnt[k]) : -1;
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-int bc_depth_lookup(const int* table, int n_buckets, double r) {
+int bc_depth_lookup(const int* table, int n_buckets, double r) try {
   if (!table || n_buckets < 1 || !(r >= 0.0)) return -1;
   long k = (long)floor(r * n_buckets + 1e-9);
   if (k > n_buckets) k = n_buckets;
   for (; k >= 1; --k)
     if (table[k] >= 0) return table[k];
   return 0;
+} catch (...) {
+  return -1;
 }
 
-bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_profile_begin(bc_model* model, unsigned kernel_mask) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   model->prof.mask = kernel_mask;
   model->prof.used = 0;
   model->prof.recs.clear();
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
-bc_status bc_profile_end(bc_model* model, double* ms, int* launches) {
-  if (!model) return fail(BC_E_INVALID, "null model");
+bc_status bc_profile_end(bc_model* model, double* ms, int* launches) try {
+  if (!live(model)) return fail(BC_E_INVALID, "null, unknown or destroyed model");
   Profiler& p = model->prof;
   p.mask = 0;
   double acc[BC_K_COUNT] = {0};
@@ -926,23 +1038,29 @@ bc_status bc_profile_end(bc_model* model, double* ms, int* launches) {
     if (launches) launches[k] = cnt[k];
   }
   return ok();
+} catch (...) {
+  return host_exception();
 }
 
 
 bc_status bc_shared_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
                                      const void* k_suf, const void* v_suf, float* out, int B,
                                      int Hq, int Hkv, int m, int n_s, int dh, float scale,
-                                     void* stream) {
+                                     void* stream) try {
   return prefix_attention(q, k_pre, v_pre, 0, k_suf, v_suf, out, B, Hq, Hkv, m, n_s, dh, scale,
                           stream);
+} catch (...) {
+  return host_exception();
 }
 
 bc_status bc_request_prefix_attention(const void* q, const void* k_pre, const void* v_pre,
                                       const void* k_suf, const void* v_suf, float* out, int B,
                                       int Hq, int Hkv, int m, int n_s, int dh, float scale,
-                                      void* stream) {
+                                      void* stream) try {
   return prefix_attention(q, k_pre, v_pre, (long)Hkv * m * dh, k_suf, v_suf, out, B, Hq, Hkv, m,
                           n_s, dh, scale, stream);
+} catch (...) {
+  return host_exception();
 }
 
 }  // extern "C"

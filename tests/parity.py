@@ -51,3 +51,29 @@ def assert_close_bf16_store(got, ref, label):
     rel = float(np.linalg.norm(got - ref) / max(np.linalg.norm(ref), 1e-30))
     say(f"  {label}: rel_fro={rel:.3e} max_abs={err.max():.3e} (bound {bound:.3e}, rms {rms:.3f})")
     assert rel <= STORE_REL_FRO and err.max() <= bound, f"{label}: rel_fro={rel:.3e} max_abs={err.max():.3e}"
+
+
+class DeviceLayersF64:
+    """The oracle's view of device-resident weights: a sequence of per-layer
+    dicts of host float64 arrays, each layer copied from the device and widened
+    exactly (bf16 -> fp64) the first time it is used, then kept.  Lets the
+    oracle run over weights that were drawn on the device."""
+
+    def __init__(self, device_layers):
+        self._dev = device_layers
+        self._host = {}
+
+    def __len__(self):
+        return len(self._dev)
+
+    def __getitem__(self, l):
+        if l < 0:
+            l += len(self._dev)
+        if l not in self._host:
+            self._host[l] = {k: (None if v is None else
+                                 v.detach().to("cpu").float().double().numpy())
+                             for k, v in self._dev[l].items()}
+        return self._host[l]
+
+    def __iter__(self):
+        return (self[l] for l in range(len(self)))

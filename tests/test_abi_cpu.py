@@ -315,3 +315,97 @@ def test_native_xxh64_matches_library(host_table):
         data = rng.integers(0, 256, size=n, dtype=np.uint8).tobytes()
         for seed in (0, 12345):
             assert host_table.bct_xxh64(data, n, seed) == xxhash.xxh64_intdigest(data, seed=seed)
+
+
+def test_misaligned_device_pointers_are_refused():
+    """Every device pointer must be 16-byte aligned (the kernels move 16-byte
+    vectors); a pointer 8 bytes off is refused before anything is enqueued."""
+    L = bc.lib()
+    MIS = FAKE + 8
+    # weights at model creation, each of the seven pointers in turn
+    for k in list(_lib._WEIGHT_KEYS) + ["b_qkv"]:
+        arr = (_lib.LayerWeights * CFG["n_layers"])()
+        for i in range(CFG["n_layers"]):
+            for kk in _lib._WEIGHT_KEYS:
+                setattr(arr[i], kk, FAKE)
+        setattr(arr[1], k, MIS)
+        c = _lib.ModelConfig(*[CFG[x] for x in ("n_layers", "hidden", "n_heads", "n_kv_heads",
+                                                 "head_dim", "ffn", "rms_eps", "rope_theta")])
+        h = C.c_void_p()
+        assert L.bc_model_create(C.byref(c), arr, 2, C.byref(h)) == -1, k
+        assert "16-byte aligned" in L.bc_last_error().decode()
+    st, h = _model()
+    big = 1 << 40
+    assert L.bc_prefix_populate(h, 1, MIS, 8, 3, FAKE, big, FAKE, big, None, None, None) == -1
+    assert "16-byte" in L.bc_last_error().decode()
+    # step inputs and outputs (refused before the key is even looked up)
+    assert L.bc_step_forward(h, 1, MIS, 2, 4, 1, FAKE, FAKE, big, None) == -1
+    assert L.bc_step_forward(h, 1, FAKE, 2, 4, 1, MIS, FAKE, big, None) == -1
+    S = L.bc_step_forward_deep
+    assert S(h, 1, MIS, 2, 4, 1, 0, FAKE, big, FAKE, FAKE, big, None) == -1
+    assert S(h, 1, FAKE, 2, 4, 1, 1, FAKE, big, MIS, FAKE, big, None) == -1
+    keys, counts = (C.c_uint64 * 1)(1), (C.c_int * 1)(2)
+    assert L.bc_step_forward_multi(h, keys, counts, 1, MIS, 4, 1, FAKE, FAKE, big, None) == -1
+    assert L.bc_profile_similarity(h, 1, MIS, 2, 4, FAKE, FAKE, big, None) == -1
+    assert L.bc_profile_similarity(h, 1, FAKE, 2, 4, MIS, FAKE, big, None) == -1
+    # attention operands, each in turn
+    for A in (L.bc_shared_prefix_attention, L.bc_request_prefix_attention):
+        for i in range(6):
+            ptrs = [FAKE] * 6
+            ptrs[i] = MIS
+            assert A(*ptrs, 2, 4, 4, 8, 4, 64, 0.1, None) == -1, i
+            assert "16-byte" in L.bc_last_error().decode()
+    # the cosine reduction
+    ws = L.bc_cosine_workspace_bytes(64)
+    assert L.bc_cosine_similarity(MIS, FAKE, 64, FAKE, FAKE, ws, None) == -1
+    assert L.bc_cosine_similarity(FAKE, FAKE, 64, MIS, FAKE, ws, None) == -1
+    L.bc_model_destroy(h)
+
+
+def test_destroyed_handle_is_refused():
+    """A handle used after bc_model_destroy is refused, never dereferenced."""
+    L = bc.lib()
+    st, h = _model()
+    assert st == 0
+    assert L.bc_model_destroy(h) == 0
+    assert L.bc_model_destroy(h) == -1
+    assert "destroyed" in L.bc_last_error().decode()
+    assert L.bc_prefix_lookup(h, 1, None, None) == -1
+    assert L.bc_prefix_invalidate(h, 1) == -1
+    n = C.c_int()
+    assert L.bc_cache_keys(h, None, 0, C.byref(n)) == -1
+    assert L.bc_step_forward(h, 1, FAKE, 2, 4, 1, FAKE, FAKE, 1 << 40, None) == -1
+    assert L.bc_step_workspace_bytes(h, 8, 2, 4, 1) == 0
+    assert L.bc_prefix_cache_bytes(h, 8, 1) == 0
+    assert L.bc_deep_store_bytes(h, 8, 2, 4, 1) == 0
+    assert L.bc_profile_begin(h, 1) == -1
+    assert L.bc_deep_store_reset(h, FAKE) == -1
+    # an unknown (never created) handle as well
+    bogus = C.c_void_p(FAKE)
+    assert L.bc_prefix_lookup(bogus, 1, None, None) == -1
+    assert L.bc_model_destroy(bogus) == -1
+
+
+def test_failed_host_allocation_leaves_table_unchanged(host_table):
+    """An allocation failure inside an insert (std::bad_alloc, which the
+    library reports as BC_E_OOM) evicts nothing and changes nothing."""
+    T = host_table
+    T.bct_fail_allocs_after.argtypes = [C.c_long]
+    t = T.bct_create(2)
+    ev = C.c_uint64()
+    assert T.bct_insert(t, 11, 1, C.byref(ev)) == 0
+    assert T.bct_insert(t, 22, 2, C.byref(ev)) == 0
+    buf = (C.c_uint64 * 4)()
+    T.bct_fail_allocs_after(0)
+    try:
+        r = T.bct_insert(t, 33, 3, C.byref(ev))
+    finally:
+        T.bct_fail_allocs_after(-1)
+    assert r == -2
+    n = T.bct_keys(t, buf, 4)
+    assert [buf[i] for i in range(n)] == [11, 22]     # nothing evicted
+    assert T.bct_lookup(t, 33) == -1 and T.bct_lookup(t, 11) == 1
+    assert T.bct_insert(t, 33, 3, C.byref(ev)) == 1 and ev.value == 11
+    n = T.bct_keys(t, buf, 4)
+    assert [buf[i] for i in range(n)] == [22, 33]
+    T.bct_destroy(t)

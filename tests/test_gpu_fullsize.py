@@ -4,17 +4,24 @@
   length (2 layers, prefix 128, suffix 64, 2 requests), against the fp64
   oracle at every reuse depth: every GEMM runs at its full N and K.
 * The full C3 step (32 layers, B 16, prefix 1536, suffix 512) in the launch
-  configuration the benchmark times, at d = 0, 8 and 32, through properties
-  that hold at any size (requests are independent given the shared cache):
-  a request's output rows are bit-identical whether it runs alone or in the
-  batch, reversing the batch reverses the outputs bit for bit, and a repeated
-  step reproduces its output exactly.
+  configuration the benchmark times, against the fp64 oracle at d = 0, 4, 8
+  and 16 on requests 0 and 15 (Eq. 4 for the shallow layers, the refresh case
+  of Eq. 5 for the deep ones); the oracle's weights are the device weights
+  widened layer by layer on first use.
+* The same step through properties that hold at any size (requests are
+  independent given the shared cache): a request's output rows are
+  bit-identical whether it runs alone or in the batch, reversing the batch
+  reverses the outputs bit for bit, and a repeated step reproduces its output.
 * Deep-layer reuse at the full C3 size (d = 8): a reuse step right after a
   refresh reproduces it bit for bit (1536 is a whole number of key tiles),
   and a request refreshed and reused alone gives its batch rows.
-* The C4 populate (prefix 8192, 8 layers of the C3 shape): the first layer's
-  cached K/V at sampled positions against the oracle, computed row by row,
-  and the first cached residual, which is the exact widening of the input.
+* The C4 populate (prefix 8192, 8 layers of the C3 shape): the cached K/V of
+  every layer and every position, and every cached residual H$[1..7],
+  against the oracle's prefix-only forward; H$[0] is the exact widening of
+  the input.
+* The cache holds exactly the bits the projection with RoPE produces: a
+  refresh step at depth d recomputes the prefix K/V of layer d from H$_d with
+  the same kernels, and writes them into the deep store bit-identical to KV$_d.
 """
 import numpy as np
 import pytest
@@ -24,7 +31,7 @@ from oracle import transformer as OT
 import paper_2606_07571_amd as bc
 from paper_2606_07571_amd import synth
 from paper_2606_07571_amd.synth import to_f64, weights_f64
-from tests.parity import assert_close, assert_close_bf16_store, say
+from tests.parity import DeviceLayersF64, assert_close, assert_close_bf16_store, say
 
 pytestmark = pytest.mark.gpu
 
@@ -55,6 +62,84 @@ def test_c3_layer_shape_every_depth():
         model.close()
 
 
+def test_c4_populate_every_layer():
+    """The C4 populate (m 8192, the first 8 layers of the C3 shape) against the
+    oracle's prefix-only forward (Sec. 5.2 miss path): K and V of every cached
+    layer, head and position (bf16 storage bound), every cached residual H$[l]
+    (fp32, the benchmark spec's tolerance), H$[0] bit-exact."""
+    cfg = synth.model_config(n_layers=8)
+    m = synth.POPULATE_C4["m"]
+    h, Hkv, dh = cfg["hidden"], cfg["n_kv_heads"], cfg["head_dim"]
+    L = synth.POPULATE_C4["n_layers_to_cache"]
+    w_cpu = synth.model_weights(cfg, 41000)
+    w_dev = synth.to_device(w_cpu)
+    xp = synth.gaussian((m, h), 41500)
+    model = bc.Model(cfg, w_dev, cache_capacity=1)
+    try:
+        key = bc.prefix_key(np.arange(m))
+        say(f"C4 populate m={m} L={L}")
+        model.populate(key, xp.cuda(), L)
+        torch.cuda.synchronize()
+        mem = model.cache_tensor(key)
+        kv_layer = Hkv * m * dh * 2
+        kv_bytes = L * 2 * kv_layer
+        h_off = model.cache_offset(m, L, 0, 2, 0, 0, 0)
+        assert h_off == kv_bytes
+        n_h = min(L + 1, cfg["n_layers"])
+        H = mem[h_off:h_off + n_h * m * h * 4].view(torch.float32).view(n_h, m, h)
+        KV = mem[:kv_bytes].view(torch.bfloat16).view(L, 2, Hkv, m, dh)
+        assert torch.isfinite(H).all() and torch.isfinite(KV.float()).all()
+        # the first cached residual is the exact widening of the prefix input
+        assert torch.equal(H[0].cpu(), xp.float())
+        say(f"C4 populate: oracle prefix-only forward of {L} layers (fp64)")
+        ref = OT.populate(to_f64(xp), weights_f64(w_cpu), cfg, L)
+        for l in range(L):
+            kv_l = KV[l].cpu().double().numpy()
+            assert_close_bf16_store(kv_l[0], ref["k"][l], f"C4 KV$ layer {l} K")
+            assert_close_bf16_store(kv_l[1], ref["v"][l], f"C4 KV$ layer {l} V")
+        for l in range(1, n_h):
+            assert_close(H[l].cpu().double().numpy(), ref["h"][l], f"C4 H$ layer {l}")
+    finally:
+        model.close()
+
+
+def test_cache_bits_equal_deep_recompute_at_depth():
+    """The cache holds exactly the bf16 bits of the projection with RoPE: a
+    refresh step at depth d recomputes layer d's prefix K/V from the cached
+    residual H$_d with the same kernels (other row positions, other tiles) and
+    writes them into the deep store; the prefix rows of every request there are
+    bit-identical to KV$_d.  At d = 0 this is the footnote of Sec. 4.2 (first-
+    layer prefix KVs depend on the prefix only).  C3 layer shape, 3 layers,
+    a prefix of 200 (not a whole number of tiles), 3 requests."""
+    cfg = synth.model_config(n_layers=3)
+    L, Hkv, dh = cfg["n_layers"], cfg["n_kv_heads"], cfg["head_dim"]
+    B, m, n_s = 3, 200, 64
+    w_dev = synth.to_device(synth.model_weights(cfg, 51000))
+    xp, xs = synth.step_inputs(cfg, B, m, n_s, 51500, device="cuda")
+    model = bc.Model(cfg, w_dev, cache_capacity=1)
+    try:
+        key = bc.prefix_key(np.arange(m) + 7)
+        model.populate(key, xp, L)
+        mem = model.cache_tensor(key)
+        for d in (0, 1, L - 1):
+            say(f"cache bits: refresh step with deep store at d={d}")
+            store = model.new_deep_store(key, B, n_s, d)
+            model.step(key, xs, d, deep="refresh", deep_store=store)
+            torch.cuda.synchronize()
+            N = m + n_s
+            for part in (0, 1):
+                c0 = model.cache_offset(m, L, d, part, 0, 0, 0)
+                cached = mem[c0:c0 + Hkv * m * dh * 2].view(torch.bfloat16).view(Hkv, m, dh)
+                s0 = model.deep_store_offset(m, B, n_s, d, d, part, 0, 0, 0, 0)
+                blk = store[s0:s0 + B * Hkv * N * dh * 2].view(torch.bfloat16).view(B, Hkv, N, dh)
+                for b in range(B):
+                    assert torch.equal(blk[b, :, :m], cached), \
+                        f"d={d} part={part} request {b}: recomputed prefix K/V differ from KV$_d"
+            del store
+    finally:
+        model.close()
+
+
 @pytest.fixture(scope="module")
 def c3_full():
     cfg = synth.model_config()
@@ -68,15 +153,49 @@ def c3_full():
     say("C3 full: populate")
     model.populate(key, xp, cfg["n_layers"])
     torch.cuda.synchronize()
-    yield cfg, model, key, xs
+    yield cfg, model, key, xs, weights, xp
     model.close()
     del weights
     torch.cuda.empty_cache()
 
 
+# depths of the full-step oracle parity: the ones the benchmark reports
+C3_DEPTHS = (0, 4, 8, 16)
+
+
+@pytest.fixture(scope="module")
+def c3_oracle(c3_full):
+    """The oracle's side of the full C3 step: its own prefix-only forward over
+    the layers the tested depths reuse (KV$ of layers 0..15, H$ 0..16), on the
+    device weights widened to fp64 on first use."""
+    cfg, model, key, xs, weights, xp = c3_full
+    W = DeviceLayersF64(weights)
+    Lc = max(C3_DEPTHS)
+    say(f"C3 full: oracle populate of {Lc} layers (fp64, m={xp.shape[0]})")
+    cache = OT.populate(to_f64(xp), W, cfg, Lc)
+    yield W, cache
+    del W, cache
+
+
+@pytest.mark.parametrize("d,b", [(d, b) for d in C3_DEPTHS for b in (0, 15)])
+def test_c3_full_size_oracle_parity(c3_full, c3_oracle, d, b):
+    """The benchmark's workload itself, element by element against the fp64
+    oracle: requests 0 and 15 of the 16-request batch at d = 0, 4, 8, 16."""
+    cfg, model, key, xs, weights, xp = c3_full
+    W, cache = c3_oracle
+    say(f"C3 full: GPU step d={d} (B={xs.shape[0]})")
+    out = torch.full(tuple(xs.shape), float("nan"), device="cuda")
+    model.step(key, xs, d, out=out)
+    torch.cuda.synchronize()
+    got = out[b].cpu().double().numpy()
+    say(f"C3 full: oracle step d={d} request {b}")
+    ref = OT.step(cache, to_f64(xs[b:b + 1]), d, W, cfg)[0]
+    assert_close(got, ref, f"C3 full step d={d} request {b}")
+
+
 @pytest.mark.parametrize("d", [0, 8, 32])
 def test_c3_full_size_request_independence(c3_full, d):
-    cfg, model, key, xs = c3_full
+    cfg, model, key, xs = c3_full[:4]
     B = xs.shape[0]
     say(f"C3 full: batch step d={d}")
     out = model.step(key, xs, d)
@@ -102,52 +221,13 @@ def test_c3_full_size_request_independence(c3_full, d):
         assert diff > 0
 
 
-def test_c4_populate_first_layer_sampled():
-    cfg = synth.model_config(n_layers=8)
-    m = synth.POPULATE_C4["m"]
-    h, Hkv, dh = cfg["hidden"], cfg["n_kv_heads"], cfg["head_dim"]
-    L = synth.POPULATE_C4["n_layers_to_cache"]
-    w_cpu = synth.model_weights(cfg, 41000)
-    w_dev = synth.to_device(w_cpu)
-    xp = synth.gaussian((m, h), 41500)
-    model = bc.Model(cfg, w_dev, cache_capacity=1)
-    try:
-        key = bc.prefix_key(np.arange(m))
-        say(f"C4 populate m={m} L={L}")
-        model.populate(key, xp.cuda(), L)
-        torch.cuda.synchronize()
-        mem = model.cache_tensor(key)
-        kv_bytes = L * 2 * Hkv * m * dh * 2
-        kv0 = mem[:2 * Hkv * m * dh * 2].view(torch.bfloat16).view(2, Hkv, m, dh)
-        h_off = model.cache_offset(m, L, 0, 2, 0, 0, 0)
-        assert h_off == kv_bytes
-        H = mem[h_off:h_off + L * m * h * 4].view(torch.float32).view(L, m, h)
-        # the first cached residual is the exact widening of the prefix input
-        assert torch.equal(H[0].cpu(), xp.float())
-        assert torch.isfinite(H).all()
-        kv_all = mem[:kv_bytes].view(torch.bfloat16)
-        assert torch.isfinite(kv_all.float()).all()
-        # layer-0 K/V of sampled positions (first, last, tile edges, random)
-        rng = np.random.default_rng(4)
-        rows = np.unique(np.concatenate([[0, 1, 63, 64, 4095, 4096, m - 2, m - 1],
-                                         rng.integers(0, m, 24)]))
-        w64 = weights_f64(w_cpu[:1])[0]
-        _, k_ref, v_ref = OT.project_qkv(to_f64(xp)[rows], w64, cfg, rows)
-        k_got = kv0[0][:, rows].cpu().double().numpy()
-        v_got = kv0[1][:, rows].cpu().double().numpy()
-        assert_close_bf16_store(k_got, k_ref, "C4 KV$ layer 0 K (sampled rows)")
-        assert_close_bf16_store(v_got, v_ref, "C4 KV$ layer 0 V (sampled rows)")
-    finally:
-        model.close()
-
-
 def test_c3_full_size_deep_reuse(c3_full):
     """Deep-layer reuse (second case of Eq. 5) at the full C3 size, d = 8.
     The prefix (1536) is a whole number of 64-key tiles, so a reuse step right
     after a refresh with the same input walks the same key tiles in the same
     order and reproduces the refresh output bit for bit; a request refreshed
     and reused on its own gives its batch rows bit for bit."""
-    cfg, model, key, xs = c3_full
+    cfg, model, key, xs = c3_full[:4]
     B, n_s = xs.shape[0], xs.shape[1]
     d = 8
     store = model.new_deep_store(key, B, n_s, d)

@@ -92,3 +92,44 @@ def test_table_floor_mean_and_lookup():
     assert P.shared_prefix_ratio(1536, 512) == 0.75
     with pytest.raises(AssertionError):
         P.build_table([0.333], [1], n_buckets=4)
+
+
+def _single_part_cos(xp, xs, layers, cfg, l, part):
+    """cos of one part (K or V) of layer l: cached prefix-only KVs against the
+    prefix rows of the un-cached forward."""
+    from oracle import transformer as TR
+    m = xp.shape[0]
+    cache = TR.populate(xp, layers, cfg, cfg["n_layers"])
+    rec = {}
+    TR.full_forward(xp, xs, layers, cfg, record=rec)
+    a = cache[part][l].ravel()
+    b = rec[part][l][:, :m].ravel()
+    return float(a @ b) / (np.linalg.norm(a) * np.linalg.norm(b))
+
+
+def test_kv_similarity_flattens_k_and_v_jointly():
+    """Footnote of Sec. 4.1: K and V of a layer form ONE flattened vector.  With
+    the layer's value projection zeroed its V part is 0, and the joint cosine
+    must equal the cosine of the K parts alone; with the key projection zeroed,
+    that of the V parts alone.  A K-only, V-only or averaged reading fails one
+    of the two (and on the untouched model all three readings differ)."""
+    cfg = _cfg(n_layers=3)
+    rng = np.random.default_rng(11)
+    layers = _weights(cfg, rng, scale_out=1 / math.sqrt(6))
+    xp, xs = rng.normal(size=(10, cfg["hidden"])), rng.normal(size=(5, cfg["hidden"]))
+    Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
+    k_rows = slice(Hq * dh, (Hq + Hkv) * dh)
+    v_rows = slice((Hq + Hkv) * dh, (Hq + 2 * Hkv) * dh)
+    l = 1
+    base = P.profile_request(xp, xs, layers, cfg)[l]
+    ck = _single_part_cos(xp, xs, layers, cfg, l, "k")
+    cv = _single_part_cos(xp, xs, layers, cfg, l, "v")
+    assert min(abs(base - ck), abs(base - cv), abs(base - (ck + cv) / 2)) > 1e-6
+    for zero, keep, part in ((v_rows, k_rows, "k"), (k_rows, v_rows, "v")):
+        lz = [dict(lw) for lw in layers]
+        w = lz[l]["w_qkv"].copy()
+        w[zero] = 0.0
+        lz[l]["w_qkv"] = w
+        sim = P.profile_request(xp, xs, lz, cfg)[l]
+        assert sim == pytest.approx(_single_part_cos(xp, xs, lz, cfg, l, part), abs=1e-12)
+        assert sim < 1 - 1e-9
