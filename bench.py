@@ -84,8 +84,9 @@ def main():
                     help="run the warmup and timed steps at --depth plus a 512 MiB copy (counter calibration) "
                          "and exit; the command profiled under rocprofv3")
     ap.add_argument("--profile-attention", action="store_true",
-                    help="run the attention configurations (5 warm-up and 5 more launches each) and exit; "
-                         "the command profiled under rocprofv3")
+                    help="run only the attention configurations, exactly as the bench times them (5 warm-up "
+                         "and 3 x 20 timed launches each), log their figures and exit; the command profiled "
+                         "under rocprofv3")
     args = ap.parse_args()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
@@ -111,13 +112,9 @@ def main():
         s = synth.ATTN_CONFIGS[cid]
         ins = synth.attention_inputs(s, 1000 * cid, device=dev)
         o = torch.empty((s.B, s.Hq, s.n_s, s.dh), dtype=torch.float32, device=dev)
-        for _ in range(10 if args.profile_attention else 5):
+        for _ in range(5):
             bc.shared_prefix_attention(*ins, out=o)
         torch.cuda.synchronize()
-        if args.profile_attention:
-            log(f"profiled C{cid}: 10 launches")
-            del ins, o
-            continue
         n, reps = 20, []
         for _ in range(3):
             e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
@@ -132,6 +129,8 @@ def main():
         attention[f"C{cid}"] = {"ms": round(t, 4), "tflops": round(fl / (t / 1e3) / 1e12, 1),
                                 "frac_of_peak": round(fl / (t / 1e3) / 1e12 / PEAK_BF16_TFLOPS, 4),
                                 "ms_range": [round(min(reps), 4), round(max(reps), 4)]}
+        if args.profile_attention:
+            log(f"profiled C{cid}: 5 warm-up + 3 x {n} timed launches, {json.dumps(attention[f'C{cid}'])}")
         del ins, o
     torch.cuda.empty_cache()
     if args.profile_attention:

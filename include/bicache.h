@@ -17,12 +17,15 @@
  *   - Device buffers are allocated and owned by the caller.  The library never
  *     allocates or frees device memory; it keeps host-side metadata only.
  *   - Tensors are dense, row-major, bf16 = IEEE bfloat16 bits (uint16), fp32 =
- *     IEEE binary32.  Device pointers must be 16-byte aligned.
+ *     IEEE binary32.  Every device pointer must be 16-byte aligned (the kernels
+ *     move 16-byte vectors); a misaligned one returns BC_E_INVALID.
  *   - `stream` is a hipStream_t passed as an opaque pointer (NULL = the null
  *     stream).  Every device operation is enqueued asynchronously on it; no
  *     call synchronizes the host.
  *   - No C++ exception crosses this boundary.  Every call returns a bc_status;
  *     bc_last_error() gives a message for the calling thread's last failure.
+ *     A failed host allocation returns BC_E_OOM; a model handle that was
+ *     destroyed (or never created) returns BC_E_INVALID.
  *     All arguments are validated before anything is enqueued, so a call that
  *     returns BC_E_INVALID / BC_E_NOT_FOUND / BC_E_STATE has no side effect.
  *   - A bc_model is not thread-safe: calls on one model must not overlap.

@@ -12,9 +12,15 @@
 //     chunks, [that request's suffix tiles of g],
 // in tiles of 64 keys staged through LDS.  A prefix tile is loaded once per
 // workgroup and consumed by all 8 waves, whatever request or query head they
-// serve, so one LDS copy of the shared prefix feeds up to 256 query rows of
-// several requests.  A suffix tile is consumed only by the waves of its
-// request.  When every request has its own prefix, the prefix tiles join the
+// serve: one LDS copy of the shared prefix feeds the workgroup's 256 query
+// rows.  Those rows span several requests only when a request brings fewer
+// than 8 chunks per KV head (GQA group size x suffix chunks < 8, e.g. two
+// 64-row suffixes); at the large shapes (suffix 256-512 rows) a workgroup
+// serves one request, and the prefix tiles shared by the requests are reused
+// from L2 and the last-level cache, not from LDS.  Putting several requests
+// into one workgroup there would make every wave walk the other requests'
+// suffix tiles masked (2.4x the tiles at the LLaDA-8B shape).  A suffix tile
+// is consumed only by the waves of its request.  When every request has its own prefix, the prefix tiles join the
 // request's part of the walk: [its prefix tiles ; its suffix tiles].
 //
 // Per wave the scores are computed transposed, S^T = K . Q^T with
