@@ -15,7 +15,8 @@
  *
  * Conventions for every entry point:
  *   - Device buffers are allocated and owned by the caller.  The library never
- *     allocates or frees device memory; it keeps host-side metadata only.
+ *     allocates or frees device memory; it keeps host-side metadata only (its
+ *     one device array is the static scratch of bc_cosine_similarity_noalloc).
  *   - Tensors are dense, row-major, bf16 = IEEE bfloat16 bits (uint16), fp32 =
  *     IEEE binary32.  Every device pointer must be 16-byte aligned (the kernels
  *     move 16-byte vectors); a misaligned one returns BC_E_INVALID.
@@ -333,6 +334,21 @@ size_t bc_cosine_workspace_bytes(long n);
  * reduction as bc_profile_similarity.  A zero vector gives NaN. */
 bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out, void* workspace,
                                size_t ws_bytes, void* stream);
+
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid hipMalloc): the same
+ * result as bc_cosine_similarity, bit for bit (same kernels, same reduction
+ * order), with no workspace argument.  The reduction's partial sums go to a
+ * static 4 MiB device array of the library, one per GPU it runs on, held
+ * until the process ends; this call allocates nothing and enqueues only the
+ * two reduction kernels.  n is a positive multiple of 8 of at most
+ * 130,146,304 elements (15,887 workgroup partials of 33 fp64 values); a
+ * larger n returns BC_E_CAPACITY before anything is enqueued.  Every call on a GPU shares that GPU's array: calls that
+ * overlap on one GPU (other streams, other threads) race and must be
+ * serialized by the caller.  Nothing carries over between calls.
+ * Other arguments and errors as bc_cosine_similarity. */
+bc_status bc_cosine_similarity_noalloc(const void* a, const void* b, long n, double* out,
+                                       void* stream);
 
 /* The shallow depth b of Sec. 4.2: the number of leading entries of
  * sims[0..n_layers) that are >= tau (0..n_layers); -1 for bad arguments.

@@ -67,6 +67,7 @@ _SIGS = {
     "bc_cosine_workspace_bytes": (C.c_size_t, [C.c_long]),
     "bc_cosine_similarity": (C.c_int, [C.c_void_p, C.c_void_p, C.c_long, C.c_void_p, C.c_void_p,
                                        C.c_size_t, C.c_void_p]),
+    "bc_cosine_similarity_noalloc": (C.c_int, [C.c_void_p, C.c_void_p, C.c_long, C.c_void_p, C.c_void_p]),
     "bc_shallow_depth": (C.c_int, [C.POINTER(C.c_double), C.c_int, C.c_double]),
     "bc_build_depth_table": (C.c_int, [C.POINTER(C.c_double), C.POINTER(C.c_int), C.c_int, C.c_int,
                                        C.POINTER(C.c_int)]),
@@ -194,6 +195,18 @@ def cosine_similarity(a, b):
     out = torch.empty((), dtype=torch.float64, device=a.device)
     _check(lib().bc_cosine_similarity(_dev(a, torch.bfloat16, "a"), _dev(b, torch.bfloat16, "b"), n,
                                       C.c_void_p(out.data_ptr()), C.c_void_p(ws.data_ptr()), wsb, _stream()))
+    return out
+
+
+def cosine_similarity_noalloc(a, b, out):
+    """cos(a, b) of two bf16 device vectors into ``out`` (a 0-d or 1-element
+    fp64 device tensor) through the entry point that allocates nothing (its
+    scratch is the library's static device array)."""
+    n = a.numel()
+    if b.numel() != n:
+        raise ValueError("operands differ in size")
+    _check(lib().bc_cosine_similarity_noalloc(_dev(a, torch.bfloat16, "a"), _dev(b, torch.bfloat16, "b"), n,
+                                              _dev(out, torch.float64, "out"), _stream()))
     return out
 
 

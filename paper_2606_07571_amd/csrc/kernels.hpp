@@ -74,6 +74,13 @@ struct CosView {
   int B;
 };
 size_t kv_cosine_partial_bytes(const CosView& v);
+// The allocation-free variant's scratch: cosine_scratch_bytes() bytes of
+// device memory per GPU (a file-scope device array); *ptr = its address on the
+// current device, looked up once per device; vectors of up to
+// cosine_scratch_max_elements() elements fit.
+size_t cosine_scratch_bytes();
+long cosine_scratch_max_elements();
+hipError_t cosine_scratch(double** ptr);
 hipError_t kv_cosine(const CosView& v, double* partial, double* out, long out_req, long out_layer,
                      hipStream_t s);
 

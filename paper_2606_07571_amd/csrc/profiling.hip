@@ -19,6 +19,8 @@
 // a time ahead of the arithmetic that consumes them; the cached chunk is read
 // once per 16 requests, so the bytes moved are (1/16 + 1) x the reference
 // copies, the reduction's floor.  Every layer goes in one launch.
+#include <mutex>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -158,6 +160,45 @@ __global__ void __launch_bounds__(kThreads) cos_final_kernel(const double* __res
 }
 
 }  // namespace
+
+// Scratch of the allocation-free cosine (bc_cosine_similarity_noalloc): the
+// per-workgroup partial sums of one reduction live in this file-scope device
+// array instead of a caller's workspace.  Every GPU the library runs on holds
+// its own copy until the process ends; every call on a GPU shares it.  Each
+// partial is written before it is read, so nothing needs clearing between
+// calls; calls that overlap on one GPU race on it.
+constexpr size_t kCosScratchBytes = 4u << 20;
+static __device__ __align__(256) double scratch[kCosScratchBytes / sizeof(double)];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+double* g_scratch_ptr[kMaxDevices] = {};
+}  // namespace
+
+size_t cosine_scratch_bytes() { return kCosScratchBytes; }
+
+long cosine_scratch_max_elements() {
+  return (long)(kCosScratchBytes / (kVals * sizeof(double))) * kChunk;
+}
+
+hipError_t cosine_scratch(double** ptr) {
+  int dev = -1;
+  hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  std::lock_guard<std::mutex> lk(g_scratch_mu);
+  if (!g_scratch_ptr[dev]) {
+    // the array's name is a host-side stand-in: only the address the runtime
+    // reports for the current device may reach a kernel
+    void* p = nullptr;
+    e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[dev] = static_cast<double*>(p);
+  }
+  *ptr = g_scratch_ptr[dev];
+  return hipSuccess;
+}
 
 size_t kv_cosine_partial_bytes(const CosView& v) {
   const long n_blocks = cdivl(v.E, kChunk) * v.P * v.H * v.L;

@@ -968,6 +968,28 @@ bc_status bc_cosine_similarity(const void* a, const void* b, long n, double* out
   return host_exception();
 }
 
+bc_status bc_cosine_similarity_noalloc(const void* a, const void* b, long n, double* out,
+                                       void* stream) try {
+  if (!a || !b || !out) return fail(BC_E_INVALID, "null argument");
+  if (n <= 0 || n % 8) return fail(BC_E_INVALID, "n=%ld must be a positive multiple of 8", n);
+  if (misaligned(a) || misaligned(b) || misaligned(out)) return fail(BC_E_INVALID, "a, b and out must be 16-byte aligned");
+  const size_t need = bc_cosine_workspace_bytes(n);
+  if (need > bc::cosine_scratch_bytes())
+    return fail(BC_E_CAPACITY, "n=%ld exceeds the %ld elements the static scratch (%zu bytes) serves",
+                n, bc::cosine_scratch_max_elements(), bc::cosine_scratch_bytes());
+  double* scr = nullptr;
+  BC_HIP(bc::cosine_scratch(&scr));
+  bc::CosView v{};
+  v.a = a;
+  v.r = b;
+  v.L = v.P = v.H = v.B = 1;
+  v.E = n;
+  BC_HIP(bc::kv_cosine(v, scr, out, 1, 1, (hipStream_t)stream));
+  return ok();
+} catch (...) {
+  return host_exception();
+}
+
 int bc_shallow_depth(const double* sims, int n_layers, double tau) try {
   if (!sims || n_layers < 0) return -1;
   int b = 0;

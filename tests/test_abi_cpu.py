@@ -409,3 +409,18 @@ def test_failed_host_allocation_leaves_table_unchanged(host_table):
     n = T.bct_keys(t, buf, 4)
     assert [buf[i] for i in range(n)] == [22, 33]
     T.bct_destroy(t)
+
+
+def test_noalloc_cosine_validation_without_device_work():
+    """The allocation-free cosine refuses, before any device work, sizes beyond
+    its static scratch (130,146,304 elements), bad sizes and misaligned or
+    null pointers."""
+    L = bc.lib()
+    N = L.bc_cosine_similarity_noalloc
+    assert N(FAKE, FAKE, 130_146_304 + 8, FAKE, None) == -6
+    assert "static scratch" in L.bc_last_error().decode()
+    assert N(FAKE, FAKE, 12, FAKE, None) == -1
+    assert N(FAKE, FAKE, 0, FAKE, None) == -1
+    assert N(FAKE + 8, FAKE, 64, FAKE, None) == -1
+    assert N(FAKE, FAKE, 64, FAKE + 8, None) == -1
+    assert N(None, FAKE, 64, FAKE, None) == -1
