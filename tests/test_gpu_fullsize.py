@@ -260,3 +260,33 @@ def test_c3_full_size_deep_reuse(c3_full):
         f"mean {diff.mean().item():.3e}")
     del store, one_store
     torch.cuda.empty_cache()
+
+
+def test_c3_full_size_reuse_step_oracle(c3_full, c3_oracle):
+    """The second case of Eq. 5 at the full C3 size, d = 8, against the fp64
+    oracle: a refresh step over the bench's batch writes the deep store, then a
+    reuse step with a changed suffix (the last 16 rows of every request replaced,
+    as denoised tokens enter) runs every layer on the suffix rows only, the deep
+    layers attending over the refreshed prefix K/V.  Request 15 against the
+    oracle's refresh (recording its deep prefix K/V) followed by its reuse
+    step."""
+    cfg, model, key, xs, weights, xp = c3_full
+    W, cache = c3_oracle
+    B, n_s = xs.shape[0], xs.shape[1]
+    d, b = 8, 15
+    xs2 = xs.clone()
+    xs2[:, -16:] = xs.flip(0)[:, -16:]
+    store = model.new_deep_store(key, B, n_s, d)
+    say(f"C3 full: GPU refresh and reuse steps d={d}")
+    model.step(key, xs, d, deep="refresh", deep_store=store)
+    out = torch.full(tuple(xs.shape), float("nan"), device="cuda")
+    model.step(key, xs2, d, out=out, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    got = out[b].cpu().double().numpy()
+    del store
+    torch.cuda.empty_cache()
+    say(f"C3 full: oracle refresh (recording the deep prefix K/V) and reuse, request {b}")
+    rec = {}
+    OT.step_one(cache, to_f64(xs[b]), d, W, cfg, record=rec)
+    ref = OT.step_reuse_one(cache, rec, to_f64(xs2[b]), d, W, cfg)
+    assert_close(got, ref, f"C3 full reuse step d={d} request {b}")
