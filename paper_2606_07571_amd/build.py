@@ -35,6 +35,8 @@ FLAGS = [
 
 
 RESOURCES = os.path.join(BUILD, "kernel_resources.json")
+# device assembly of the GEMMs, checked by the CPU tests (M0 discipline)
+GEMM_ASM = os.path.join(BUILD, "gemm_device.s")
 
 
 def _parse_resources(stderr):
@@ -70,6 +72,14 @@ def _compile(src):
     return obj, _parse_resources(r.stderr)
 
 
+def _gemm_asm():
+    cmd = [HIPCC, *FLAGS, "-S", "--cuda-device-only", os.path.join(CSRC, "gemm.hip"), "-o", GEMM_ASM]
+    r = subprocess.run(cmd, capture_output=True, text=True)
+    if r.returncode != 0:
+        raise RuntimeError(f"gemm.hip device assembly failed:\n{r.stderr}")
+    return GEMM_ASM
+
+
 def build_host_lib():
     os.makedirs(os.path.dirname(HOST_LIB), exist_ok=True)
     cxx = shutil.which("g++") or "c++"
@@ -82,8 +92,10 @@ def build_host_lib():
 
 def build(verbose=True):
     os.makedirs(BUILD, exist_ok=True)
-    with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES), os.cpu_count() or 4)) as ex:
+    with cf.ThreadPoolExecutor(max_workers=min(len(SOURCES) + 1, os.cpu_count() or 4)) as ex:
+        asm = ex.submit(_gemm_asm)
         results = list(ex.map(_compile, SOURCES))
+        asm.result()
     objs = [o for o, _ in results]
     resources = {}
     for _, res in results:

@@ -1,19 +1,24 @@
 // bf16 GEMMs on gfx950 MFMA with the epilogues of the transformer layer:
 // residual add (O and down projections), SwiGLU (gate/up projection) and the
 // fused Q/K/V projection with optional bias, rotate-half RoPE and head-major
-// scatter (which,
-// during populate, writes the prefix K/V straight into the cache entry).
+// scatter (which, during populate, writes the prefix K/V straight into the
+// cache entry).
 //
 // C[M, N] = A[M, K] . W[N, K]^T.  Both operands are K-contiguous, so every
 // MFMA operand fragment is one 16-byte LDS read per lane and no transpose is
 // needed anywhere.
 //
-// Tiling: a workgroup computes a 256 x 256 tile with 8 waves, each a 64 x 128
-// sub-tile of 32x32 MFMA blocks (v_mfma_f32_32x32x16_bf16); K advances in
-// steps of 64 through a double-buffered LDS tile pair (see gemm_pp_kernel for
-// the schedule).  LDS rows are 128 bytes (64 bf16) with an XOR-swizzled
-// 16-byte chunk index (see swz), conflict-free for both the fills and the
-// fragment reads.
+// Tiling: a workgroup of 4 waves (one per SIMD) computes a 256 x 256 tile,
+// each wave a 128 x 128 sub-tile of 4 x 4 32x32 blocks
+// (v_mfma_f32_32x32x16_bf16, accumulators in the 256 accumulation registers).
+// K advances in steps of 64 through two LDS tile buffers; operand tiles are
+// loaded straight into LDS (buffer loads with the LDS bit), so no register
+// staging is needed.  LDS rows are 128 bytes (64 bf16) with an XOR-swizzled
+// 16-byte chunk index (see swz), conflict-free for the fragment reads.  After
+// the K loop the tile buffers become the epilogue's staging area: every
+// epilogue writes its outputs as whole 16-byte row chunks.
+#include <type_traits>
+
 #include "device_common.hpp"
 #include "kernels.hpp"
 
@@ -35,22 +40,27 @@ struct GemmArgs {
 
 // LDS serves 128-bit accesses 16 lanes (256 bytes, 64 banks) at a time; with
 // 128-byte rows two consecutive rows fill the 64 banks, so the chunk index is
-// XOR-ed with (row >> 1) & 7: the 16 rows read together by a fragment load, and
-// the 2 rows x 8 chunks written together by a fill, all land on distinct banks.
+// XOR-ed with (row >> 1) & 7: the 16 rows read together by a fragment load all
+// land on distinct banks.
 __device__ __forceinline__ int swz(int row, int kc) { return row * BK + ((kc ^ ((row >> 1) & 7)) << 3); }
 
 // ---------------------------------------------------------------- epilogues
 // Each epilogue says how many BN-wide tiles cover its output (tiles_n), which
-// row of W feeds tile-local B row r (w_row, -1 = zero row) and how the wave's
-// accumulators are written (apply).  Accumulator (i, j, e) of lane l holds
-// C[row0 + i*32 + 8*(e/4) + 4*(l/32) + e%4][col0 + j*32 + l%32].
+// row of W feeds tile-local B row r (w_row, -1 = zero row) and how a wave's
+// accumulators leave (apply).  Accumulator (i, j, e) of lane l holds
+// C[row0 + i*32 + 8*(e/4) + 4*(l/32) + e%4][col0 + j*32 + l%32]: a lane holds
+// columns, so every epilogue first writes its values to its slot of LDS and
+// reads them back as row chunks.  `half` is one of the two 64 KiB halves of
+// the tile buffers (shared by two waves), `slot` the wave's index in it.
 
-// R += A . W^T: the accumulators start from the residual tile (init), so the
-// residual is read while the first K steps load and the epilogue only writes.
+// R += A . W^T, fp32.  32 rows at a time: the accumulators of a 32-row block go
+// to LDS (row pitch 4 TN + 32 bytes, so the two half-waves of a write land on
+// disjoint banks), come back as 4-column row chunks, are added to the residual
+// chunks (loaded one block ahead) and stored.  Whole chunks with a row stride
+// that is a multiple of 4 move as 16-byte vectors, others element by element.
 struct EpiResidual {
   float* R;
   int ldr, N;
-  static constexpr bool kInit = true;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(N, BN); }
   __host__ __device__ int w_rows() const { return N; }
   template <int BN, int TN>
@@ -58,49 +68,76 @@ struct EpiResidual {
     int n = tn * BN + r;
     return n < N ? n : -1;
   }
-  template <int BN, int TN, int FM, int FN>
-  __device__ __forceinline__ void init(f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn, int lane) const {
-    const int col0 = tn * BN + wn * TN + (lane & 31);
-#pragma unroll
-    for (int i = 0; i < FM; ++i)
-#pragma unroll
-      for (int e = 0; e < 16; ++e) {
-        const int row = row0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        const float* rp = R + (long)(row < M ? row : 0) * ldr;
-#pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int col = col0 + j * 32;
-          acc[i][j][e] = (row < M && col < N) ? rp[col] : 0.f;
-        }
-      }
-  }
+  static constexpr int kSlotBytes(int TN, int) { return 32 * (TN * 4 + 32); }
   template <int BN, int TN, int FM, int FN>
   __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
-                        int lane) const {
-    const int col0 = tn * BN + wn * TN + (lane & 31);
+                                        int lane, char* half, int slot) const {
+    const int colw = tn * BN + wn * TN;
+    constexpr int P = TN * 4 + 32;
+    char* lds = half + slot * (32 * P);
+    constexpr int CPR = TN / 4;    // 16-byte chunks per row
+    constexpr int RPI = 64 / CPR;  // rows per instruction
+    constexpr int NR = 32 / RPI;   // instructions per 32-row block
+    const int cr = lane / CPR, col = colw + (lane % CPR) * 4;
+    const bool whole = col + 4 <= N && (ldr & 3) == 0;
+    f32x4 rv[2][NR];
+    auto load_r = [&](int i, int set) __attribute__((always_inline)) {
 #pragma unroll
-    for (int i = 0; i < FM; ++i)
+      for (int n = 0; n < NR; ++n) {
+        const int row = row0 + i * 32 + n * RPI + cr;
+        const float* rp = R + (long)row * ldr + col;
+        f32x4 x = {0.f, 0.f, 0.f, 0.f};
+        if (row < M) {
+          if (whole) {
+            x = *reinterpret_cast<const f32x4*>(rp);
+          } else {
+#pragma unroll
+            for (int u = 0; u < 4; ++u)
+              if (col + u < N) x[u] = rp[u];
+          }
+        }
+        rv[set][n] = x;
+      }
+    };
+    load_r(0, 0);
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+      if (i + 1 < FM) load_r(i + 1, (i + 1) & 1);
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int row = row0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (row >= M) continue;
-        float* rp = R + (long)row * ldr;
+        const int r = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
 #pragma unroll
-        for (int j = 0; j < FN; ++j) {
-          const int col = col0 + j * 32;
-          if (col < N) rp[col] = acc[i][j][e];
+        for (int j = 0; j < FN; ++j)
+          *reinterpret_cast<float*>(lds + r * P + (j * 32 + (lane & 31)) * 4) = acc[i][j][e];
+      }
+#pragma unroll
+      for (int n = 0; n < NR; ++n) {
+        const int r = n * RPI + cr, row = row0 + i * 32 + r;
+        const f32x4 v = *reinterpret_cast<const f32x4*>(lds + r * P + (lane % CPR) * 16) + rv[i & 1][n];
+        if (row >= M) continue;
+        float* rp = R + (long)row * ldr + col;
+        if (whole) {
+          *reinterpret_cast<f32x4*>(rp) = v;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 4; ++u)
+            if (col + u < N) rp[u] = v[u];
         }
       }
+    }
   }
 };
 
-// Gate and up rows of the same output columns are interleaved inside each
-// wave's sub-tile: the first TN/2 B rows of a wave are gate rows, the last TN/2
-// are the up rows of the same columns, so silu(g) * u is lane-local.
+// act = silu(g) * u, bf16.  Gate and up rows of the same output columns are
+// interleaved inside each wave's sub-tile: the first TN/2 B rows of a wave are
+// gate rows, the last TN/2 the up rows of the same columns, so the product is
+// lane-local.  silu(g) * u = g u / (1 + e^-g) with a hardware reciprocal.  The
+// wave's (FM*32) x (TN/2) block goes through LDS (row pitch TN + 16 bytes) and
+// leaves as 16-byte stores of 8-column row chunks; a chunk not whole inside F
+// (or F not a multiple of 8) is stored element by element.
 struct EpiSwiGLU {
   bf16* act;
   int F;
-  static constexpr bool kInit = false;
   __host__ __device__ int tiles_n(int BN) const { return cdiv(F, BN / 2); }
   __host__ __device__ int w_rows() const { return 2 * F; }
   template <int BN, int TN>
@@ -110,31 +147,57 @@ struct EpiSwiGLU {
     const int col = tn * (BN / 2) + wn * (TN / 2) + within;
     return col < F ? half * F + col : -1;
   }
+  static constexpr int kSlotBytes(int TN, int TM) { return TM * (TN + 16); }
   template <int BN, int TN, int FM, int FN>
   __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
-                        int lane) const {
-    const int col0 = tn * (BN / 2) + wn * (TN / 2) + (lane & 31);
+                                        int lane, char* half, int slot) const {
+    const int colw = tn * (BN / 2) + wn * (TN / 2);
+    constexpr int P = TN + 16;
+    char* lds = half + slot * (FM * 32 * P);
 #pragma unroll
     for (int i = 0; i < FM; ++i)
 #pragma unroll
       for (int e = 0; e < 16; ++e) {
-        const int row = row0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-        if (row >= M) continue;
-        bf16* op = act + (long)row * F;
+        const int r = i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
 #pragma unroll
         for (int j = 0; j < FN / 2; ++j) {
-          const int col = col0 + j * 32;
-          if (col >= F) continue;
           const float g = acc[i][j][e], u = acc[i][j + FN / 2][e];
-          op[col] = to_bf16(g / (1.f + __expf(-g)) * u);
+          *reinterpret_cast<bf16*>(lds + r * P + (j * 32 + (lane & 31)) * 2) =
+              to_bf16(g * u * __builtin_amdgcn_rcpf(1.f + __expf(-g)));
         }
       }
+    constexpr int CPR = TN / 16;   // 16-byte chunks per row
+    constexpr int RPP = 64 / CPR;  // rows per pass
+    const int col = colw + (lane % CPR) * 8;
+    const bool whole = col + 8 <= F && (F & 7) == 0;
+#pragma unroll
+    for (int p = 0; p < FM * 32 / RPP; ++p) {
+      const int r = p * RPP + lane / CPR;
+      const bf16x8 v = *reinterpret_cast<const bf16x8*>(lds + r * P + (lane % CPR) * 16);
+      if (row0 + r >= M) continue;
+      bf16* op = act + (long)(row0 + r) * F + col;
+      if (whole) {
+        *reinterpret_cast<bf16x8*>(op) = v;
+      } else {
+#pragma unroll
+        for (int u = 0; u < 8; ++u)
+          if (col + u < F) op[u] = v[u];
+      }
+    }
   }
 };
 
+// Q/K/V heads, bf16, head-major.  Output column block j of W (head j, DH rows)
+// goes to Q head j (j < Hq), K head j - Hq (j < Hq + Hkv) or V head
+// j - Hq - Hkv; the bias (one per column, or null) is added first, then Q and K
+// are rotated (rotate-half RoPE: dims i and i + DH/2 form a pair) with the
+// fp32 tables cos_t/sin_t [pos][DH/2].  A wave's sub-tile holds whole heads.
+// 32 rows at a time go through LDS in fp32 (row pitch 4 TN + 32 bytes); reading
+// back, a lane takes 8 rotation pairs (i, i + DH/2) of one row: 16-byte LDS
+// reads, 16-byte loads of the cos/sin rows, and two 16-byte bf16 stores
+// (element by element if a part's strides are not multiples of 8).
 template <int DH>
 struct EpiQKV {
-  static constexpr bool kInit = false;
   bf16* q;
   bf16* k;
   bf16* v;
@@ -151,104 +214,176 @@ struct EpiQKV {
     int n = tn * BN + r;
     return n < ncols() ? n : -1;
   }
+  static constexpr int kSlotBytes(int TN, int) { return 32 * (TN * 4 + 32); }
   template <int BN, int TN, int FM, int FN>
   __device__ __forceinline__ void apply(const f32x16 (&acc)[FM][FN], int M, int tn, int row0, int wn,
-                        int lane) const {
-    static_assert(TN % DH == 0, "a wave sub-tile must hold whole heads");
-    constexpr int BPH = DH / 32;  // 32-column blocks per head
+                                        int lane, char* half, int slot) const {
+    static_assert(TN % DH == 0 && DH % 16 == 0, "a wave sub-tile must hold whole heads");
+    const int col0 = tn * BN + wn * TN;
+    const int head0 = col0 / DH;
+    const bool vec = ((q_sb | q_sh | k_sb | k_sh | v_sb | v_sh) & 7) == 0;
+    constexpr int P = TN * 4 + 32;
+    char* lds = half + slot * (32 * P);
+    float bj[FN];
 #pragma unroll
-    for (int hh = 0; hh < TN / DH; ++hh) {
-      const int head_g = (tn * BN + wn * TN) / DH + hh;
-      if (head_g >= Hq + 2 * Hkv) continue;
-      bf16* base;
-      long sb, sh;
-      int head;
-      bool rot = true;
-      if (head_g < Hq) {
-        base = q; sb = q_sb; sh = q_sh; head = head_g;
-      } else if (head_g < Hq + Hkv) {
-        base = k; sb = k_sb; sh = k_sh; head = head_g - Hq;
-      } else {
-        base = v; sb = v_sb; sh = v_sh; head = head_g - Hq - Hkv; rot = false;
+    for (int j = 0; j < FN; ++j) {
+      const int c = col0 + j * 32 + (lane & 31);
+      bj[j] = bias && c < ncols() ? bf16_to_f32(bias[c]) : 0.f;
+    }
+    constexpr int GPH = DH / 16;          // 8-pair groups per head
+    constexpr int LPR = (TN / DH) * GPH;  // lanes per row
+    constexpr int RPI = 64 / LPR;         // rows per instruction
+    const int g = lane % LPR, hh = g / GPH, d0 = (g % GPH) * 8;
+    const int c1 = hh * DH + d0, c2 = c1 + DH / 2;
+    const int head_g = head0 + hh;
+    bf16* base;
+    long sb, sh;
+    int head;
+    bool rot = true;
+    if (head_g < Hq) {
+      base = q; sb = q_sb; sh = q_sh; head = head_g;
+    } else if (head_g < Hq + Hkv) {
+      base = k; sb = k_sb; sh = k_sh; head = head_g - Hq;
+    } else {
+      base = v; sb = v_sb; sh = v_sh; head = head_g - Hq - Hkv; rot = false;
+    }
+#pragma unroll
+    for (int i = 0; i < FM; ++i) {
+#pragma unroll
+      for (int e = 0; e < 16; ++e) {
+        const int r = 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
+#pragma unroll
+        for (int j = 0; j < FN; ++j) {
+          float x = acc[i][j][e];
+          if (bias) x += bj[j];
+          *reinterpret_cast<float*>(lds + r * P + (j * 32 + (lane & 31)) * 4) = x;
+        }
       }
 #pragma unroll
-      for (int i = 0; i < FM; ++i)
+      for (int n = 0; n < 32 / RPI; ++n) {
+        const int r = n * RPI + lane / LPR, row = row0 + i * 32 + r;
+        const f32x4 a0 = *reinterpret_cast<const f32x4*>(lds + r * P + c1 * 4);
+        const f32x4 a1 = *reinterpret_cast<const f32x4*>(lds + r * P + c1 * 4 + 16);
+        const f32x4 b0 = *reinterpret_cast<const f32x4*>(lds + r * P + c2 * 4);
+        const f32x4 b1 = *reinterpret_cast<const f32x4*>(lds + r * P + c2 * 4 + 16);
+        if (row >= M || head_g >= Hq + 2 * Hkv) continue;
+        const int b = row / n_seq, t = row - b * n_seq;
+        const float x1[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+        const float x2[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+        bf16x8 o1, o2;
+        if (rot) {
+          const float* ct = cos_t + (long)(pos0 + t) * (DH / 2) + d0;
+          const float* st = sin_t + (long)(pos0 + t) * (DH / 2) + d0;
+          const f32x4 c0 = *reinterpret_cast<const f32x4*>(ct), c4 = *reinterpret_cast<const f32x4*>(ct + 4);
+          const f32x4 s0 = *reinterpret_cast<const f32x4*>(st), s4 = *reinterpret_cast<const f32x4*>(st + 4);
+          const float cc[8] = {c0.x, c0.y, c0.z, c0.w, c4.x, c4.y, c4.z, c4.w};
+          const float ss[8] = {s0.x, s0.y, s0.z, s0.w, s4.x, s4.y, s4.z, s4.w};
 #pragma unroll
-        for (int e = 0; e < 16; ++e) {
-          const int row = row0 + i * 32 + 8 * (e >> 2) + 4 * (lane >> 5) + (e & 3);
-          if (row >= M) continue;
-          const int b = row / n_seq, t = row - b * n_seq;
-          bf16* dst = base + b * sb + head * sh + (long)t * DH;
-          const float* ct = cos_t + (long)(pos0 + t) * (DH / 2);
-          const float* st = sin_t + (long)(pos0 + t) * (DH / 2);
+          for (int u = 0; u < 8; ++u) {
+            o1[u] = to_bf16(x1[u] * cc[u] - x2[u] * ss[u]);
+            o2[u] = to_bf16(x2[u] * cc[u] + x1[u] * ss[u]);
+          }
+        } else {
 #pragma unroll
-          for (int jj = 0; jj < BPH / 2; ++jj) {
-            const int d1 = jj * 32 + (lane & 31);
-            float x1 = acc[i][hh * BPH + jj][e];
-            float x2 = acc[i][hh * BPH + jj + BPH / 2][e];
-            if (bias) {
-              x1 += bf16_to_f32(bias[head_g * DH + d1]);
-              x2 += bf16_to_f32(bias[head_g * DH + d1 + DH / 2]);
-            }
-            float y1 = x1, y2 = x2;
-            if (rot) {
-              const float c = ct[d1], s = st[d1];
-              y1 = x1 * c - x2 * s;
-              y2 = x2 * c + x1 * s;
-            }
-            dst[d1] = to_bf16(y1);
-            dst[d1 + DH / 2] = to_bf16(y2);
+          for (int u = 0; u < 8; ++u) {
+            o1[u] = to_bf16(x1[u]);
+            o2[u] = to_bf16(x2[u]);
           }
         }
+        bf16* dst = base + b * sb + head * sh + (long)t * DH + d0;
+        if (vec) {
+          *reinterpret_cast<bf16x8*>(dst) = o1;
+          *reinterpret_cast<bf16x8*>(dst + DH / 2) = o2;
+        } else {
+#pragma unroll
+          for (int u = 0; u < 8; ++u) {
+            dst[u] = o1[u];
+            dst[u + DH / 2] = o2[u];
+          }
+        }
+      }
     }
   }
 };
 
-// ---------------------------------------------------------------- ping-pong kernel
-// Same 256 x 256 tile and 64 x 128 wave sub-tiles, but the two waves that
-// share a SIMD never do the same kind of work at the same time.  Waves 0-3
-// (group 0, columns 0-127 of the tile) and waves 4-7 (group 1, columns
-// 128-255) run the same program, group 1 one barrier-phase behind.  Each half
-// K step (32 of K) is a memory phase -- read this half step's fragments from
-// LDS, write half of the next K step's tile into the free LDS buffer and
-// issue the global loads of the same half of the K step after it -- then a
-// compute phase of 16 MFMAs, with a workgroup barrier between phases.  While
-// one group issues its MFMAs the other group's LDS and global traffic runs,
-// so the matrix pipe of every SIMD is fed alternately by its two waves, and
-// both memory phases carry the same load.
-//
-// LDS tiles are double-buffered: K step k+1 is written during step k (after
-// every wave has finished reading that buffer's previous tile, step k-1) and
-// is first read at step k+1.  Group 0 fetches and writes the A tile, group 1
-// the W tile, 8 chunks of 16 bytes per lane per K step, through buffer loads:
-// A's descriptor starts at the tile's first row and covers its valid rows, W
-// rows that an epilogue maps to nothing get an offset past W's end, so rows
-// outside the matrices read as zero with no selects.  Each load has four
-// phases (one K step) to land before its chunk is written to LDS.
-template <class Epi>
-__global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
-  constexpr int BM = 256, BN = 256, TM = 64, TN = 128, FM = 2, FN = 4;
-  constexpr int PER = 8, HPER = 4;  // 16-byte chunks per lane per K step, per half
-  constexpr int RSRC_W3 = 0x00020000;  // raw buffer, 32-bit dwords (gfx9 family)
-  constexpr uint32_t kNoRow = 0x80000000u;  // offset past every descriptor's range
+// ---------------------------------------------------------------- loads into LDS
+typedef int i32x4 __attribute__((ext_vector_type(4)));
 
-  __shared__ __attribute__((aligned(16))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(16))) bf16 sB[2][BN * BK];
+// 16 bytes per lane from a buffer straight into LDS: lane l's chunk lands at
+// LDS byte address M0 + inst_offset + 16 l, and is read from the buffer at
+// voffset + soffset + inst_offset (out-of-range offsets read as zero).  Loads
+// go in groups of four sharing one M0 value: sub 0 sets M0 (one wait state
+// before the load reads it), subs 1-3 add 1, 2, 3 KiB through the instruction
+// offset, which the caller has subtracted from their voffset.  Written as
+// inline assembly so that the compiler does not count these loads: it would
+// otherwise wait for every one of them before any LDS read.  The kernel waits
+// for them itself (vmcnt) before the barrier that publishes a tile.  M0 is
+// written only here; nothing else in the kernels reads it.
+#pragma clang diagnostic push
+#pragma clang diagnostic ignored "-Winline-asm"
+__device__ __forceinline__ void load_lds16(i32x4 rsrc, uint32_t voff, uint32_t soff, uint32_t lds, int sub) {
+  switch (sub) {
+    case 0:
+      asm volatile("s_mov_b32 m0, %3\n\ts_nop 0\n\tbuffer_load_dwordx4 %0, %1, %2 offen lds"
+                   :: "v"(voff), "s"(rsrc), "s"(soff), "s"(lds) : "memory", "m0");
+      break;
+    case 1:
+      asm volatile("buffer_load_dwordx4 %0, %1, %2 offen offset:1024 lds"
+                   :: "v"(voff), "s"(rsrc), "s"(soff) : "memory");
+      break;
+    case 2:
+      asm volatile("buffer_load_dwordx4 %0, %1, %2 offen offset:2048 lds"
+                   :: "v"(voff), "s"(rsrc), "s"(soff) : "memory");
+      break;
+    default:
+      asm volatile("buffer_load_dwordx4 %0, %1, %2 offen offset:3072 lds"
+                   :: "v"(voff), "s"(rsrc), "s"(soff) : "memory");
+      break;
+  }
+}
+#pragma clang diagnostic pop
+
+// Waits for this wave's loads into LDS and its LDS reads, then the workgroup
+// barrier, in one statement so that no LDS access moves across it.
+__device__ __forceinline__ void wait_loads_barrier() {
+  asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
+
+// ---------------------------------------------------------------- kernel
+// K step k (64 of K) uses LDS buffer k % 2 and is four substeps of 16 of K;
+// a "phase" is the 16 MFMAs of one substep.  Each K step starts right after
+// the barrier that published its tiles: its first phase runs the last substep
+// of step k - 1 (fragments already in registers) beside the first fragment
+// reads of step k, and the loads of step k + 1 go to the other buffer, whose
+// last reads (step k - 1) all happened before that barrier.  Substeps 0-2 of
+// step k each run beside the next substep's fragment reads; the barrier that
+// closes the step follows once this wave's loads have landed.  The 16 loads of
+// a K step (8 A, 8 W per wave) are spread one per two MFMAs over the first two
+// phases: issued in one phase they stall the wave (the address unit takes them
+// slower than the phase issues them); issued later they have too little time
+// to land.  Every phase is a fixed sequence: sched_barrier keeps the compiler
+// from regrouping it.
+template <class Epi>
+__global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
+  constexpr int BM = 256, BN = 256, TM = 128, TN = 128, FM = 4, FN = 4;
+  constexpr uint32_t kNoRow = 0x80000000u;  // offset past every buffer range
+  static_assert(2 * Epi::kSlotBytes(TN, TM) <= BM * BK * 2 * 2, "epilogue staging exceeds half the tile buffers");
+
+  __shared__ __attribute__((aligned(1024))) bf16 sA[2][BM * BK];
+  __shared__ __attribute__((aligned(1024))) bf16 sB[2][BN * BK];
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-  const int grp = wave >> 2;          // 0: loads A, computes columns 0-127; 1: W, 128-255
-  const int wm = wave & 3, wn = grp;  // the two waves on a SIMD are w and w + 4
+  const int wm = wave & 1, wn = wave >> 1;
 
   const int tiles_m = cdiv(a.M, BM), tiles_n = epi.tiles_n(BN);
   const int lid = xcd_remap(blockIdx.x, gridDim.x);
   // Tile order: each die takes a contiguous range of tiles, swept in groups
-  // of GM row tiles, column-major inside a group, so the 32 tiles a die runs
-  // at once share A and W panels in its L2.  When a row of tiles is at most
-  // 32 wide (the O and down projections: N = h), whole rows run at once
-  // (GM = 1): every A panel is then read from HBM once and the small W is
-  // re-read from the last-level cache (measured +2% and +4% on the O and down
-  // shapes against GM = 8, which suits the wide QKV and gate/up outputs).
+  // of GM row tiles, column-major inside a group, so the tiles a die runs at
+  // once share A and W panels in its L2.  When a row of tiles is at most 32
+  // wide (the O and down projections: N = h), whole rows run at once (GM = 1):
+  // every A panel is then read from HBM once and the small W is re-read from
+  // the last-level cache.
   const int GM = tiles_n <= 32 ? 1 : 8;
   const int per_group = GM * tiles_n;
   const int first_m = (lid / per_group) * GM;
@@ -257,43 +392,39 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
   const int tn = (lid % per_group) / gsz;
   const int m0 = tm * BM;
 
-  // this lane's chunks of its group's operand tile: chunk p covers tile row
-  // lane/8 + 8*wm + 32*p, 16-byte column chunk lane%8
-  const int kc = lane & 7;
-  uint32_t voff[PER];
-  __amdgpu_buffer_rsrc_t rsrc;
-  if (grp == 0) {
-    const int rows = min(BM, a.M - m0);
-    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(a.A + (long)m0 * a.lda), (short)0,
-                                             rows * a.lda * 2, RSRC_W3);
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int r = (lane >> 3) + 8 * wm + 32 * p;
-      voff[p] = r < rows ? (uint32_t)(r * a.lda + kc * 8) * 2u : kNoRow;
-    }
-  } else {
-    rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(a.W), (short)0, a.w_bytes, RSRC_W3);
-#pragma unroll
-    for (int p = 0; p < PER; ++p) {
-      const int r = (lane >> 3) + 8 * wm + 32 * p;
-      const int gr = epi.template w_row<BN, TN>(tn, r);
-      voff[p] = gr >= 0 ? (uint32_t)(gr * a.ldw + kc * 8) * 2u : kNoRow;
-    }
+  // Load q < 8 of wave w fills LDS chunks [(8w + q) 64, +64) of the A tile,
+  // q >= 8 the same chunks of the W tile: lane l writes tile row
+  // r = 8 (8w + q % 8) + l / 8 at swizzled chunk column l % 8, so it fetches
+  // the logical chunk (l % 8) ^ ((r >> 1) & 7) of that row.  A's buffer starts
+  // at the tile's first row and covers its valid rows; W rows an epilogue maps
+  // to nothing get an offset past W's range, so rows outside the matrices read
+  // as zero with no selects.  K advances in the scalar offset.
+  const int rows_a = min(BM, a.M - m0);
+  i32x4 ra, rw;
+  {
+    auto u = [](int x) { return __builtin_amdgcn_readfirstlane(x); };
+    const uint64_t pa = (uint64_t)(a.A + (long)m0 * a.lda), pw = (uint64_t)a.W;
+    ra = i32x4{u((int)pa), u((int)(pa >> 32)), u(rows_a * a.lda * 2), 0x00020000};
+    rw = i32x4{u((int)pw), u((int)(pw >> 32)), u(a.w_bytes), 0x00020000};
   }
-  bf16* const dst0 = grp == 0 ? &sA[0][0] : &sB[0][0];
-  u32x4 stage[PER];
-  auto fetch = [&](int k0, int h) __attribute__((always_inline)) {
+  uint32_t voff[16];
 #pragma unroll
-    for (int p = h * HPER; p < (h + 1) * HPER; ++p)
-      stage[p] = __builtin_amdgcn_raw_buffer_load_b128(rsrc, voff[p], k0 * 2, 0);
-  };
-  auto stash = [&](int buf, int h) __attribute__((always_inline)) {
-    bf16* dst = dst0 + buf * (BM * BK);
-#pragma unroll
-    for (int p = h * HPER; p < (h + 1) * HPER; ++p) {
-      const int r = (lane >> 3) + 8 * wm + 32 * p;
-      *reinterpret_cast<u32x4*>(&dst[swz(r, kc)]) = stage[p];
-    }
+  for (int q = 0; q < 8; ++q) {
+    const int r = 8 * (8 * wave + q) + (lane >> 3);
+    const int kc = (lane & 7) ^ ((r >> 1) & 7);
+    // rows r >= 8 (q % 4) hold at least (q % 4) KiB of offset (K >= 64), so
+    // subtracting the group's instruction offset cannot wrap
+    voff[q] = r < rows_a ? (uint32_t)(r * a.lda + kc * 8) * 2u - (q & 3) * 1024u : kNoRow;
+    const int gr = epi.template w_row<BN, TN>(tn, r);
+    voff[8 + q] = gr >= 0 ? (uint32_t)(gr * a.ldw + kc * 8) * 2u - (q & 3) * 1024u : kNoRow;
+  }
+  const uint32_t ldsA = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16*)&sA[0][0];
+  const uint32_t ldsB = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16*)&sB[0][0];
+  constexpr uint32_t kBuf = BM * BK * 2;  // bytes of one tile buffer
+  auto load = [&](int q, int buf, int k0) __attribute__((always_inline)) {
+    const uint32_t lds = (q < 8 ? ldsA : ldsB) + buf * kBuf + (8 * wave + (q & 4)) * 1024;
+    load_lds16(q < 8 ? ra : rw, voff[q], __builtin_amdgcn_readfirstlane(k0 * 2),
+               __builtin_amdgcn_readfirstlane(lds), q & 3);
   };
 
   f32x16 acc[FM][FN];
@@ -302,72 +433,80 @@ __global__ void __launch_bounds__(512) gemm_pp_kernel(GemmArgs a, Epi epi) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
 
-  bf16x8 fa[2][FM], fb[2][FN];
-  auto read_frags = [&](int cur, int h) __attribute__((always_inline)) {
+  // fragment f < 4: A block f, f >= 4: W block f - 4, of substep s
+  bf16x8 fr[2][8];
+  auto read_frag = [&](int buf, int s, int set, int f) __attribute__((always_inline)) {
+    const int kci = s * 2 + (lane >> 5);
+    if (f < 4)
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sA[buf][swz(wm * TM + f * 32 + (lane & 31), kci)]);
+    else
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sB[buf][swz(wn * TN + (f - 4) * 32 + (lane & 31), kci)]);
+  };
+  // reads in the order the next phase's MFMAs need them
+  constexpr int kReadOrder[8] = {0, 4, 5, 6, 7, 1, 2, 3};
+  // One phase: the 16 MFMAs of the fragments in set mset (if MMA), the 8
+  // fragment reads of substep rs of buffer rbuf into set rset (if RD), and NG
+  // load groups (4 loads each), starting at group g0, of the K step at k0 into
+  // buffer dbuf, one load per 16 / (4 NG) MFMAs.
+  auto phase = [&](auto MMA, auto RD, auto NG, int mset, int rbuf, int rs, int rset, int g0, int dbuf, int k0)
+      __attribute__((always_inline)) {
+    constexpr int ng = decltype(NG)::value;
 #pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2) {
-      const int kci = (2 * h + k2) * 2 + (lane >> 5);
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-        fa[k2][i] = *reinterpret_cast<const bf16x8*>(&sA[cur][swz(wm * TM + i * 32 + (lane & 31), kci)]);
-#pragma unroll
-      for (int j = 0; j < FN; ++j)
-        fb[k2][j] = *reinterpret_cast<const bf16x8*>(&sB[cur][swz(wn * TN + j * 32 + (lane & 31), kci)]);
+    for (int q = 0; q < 16; ++q) {
+      if constexpr (decltype(MMA)::value)
+        acc[q >> 2][q & 3] = mfma_32x32x16(fr[mset][q >> 2], fr[mset][4 + (q & 3)], acc[q >> 2][q & 3]);
+      if constexpr (decltype(RD)::value)
+        if ((q & 1) == 0) read_frag(rbuf, rs, rset, kReadOrder[q >> 1]);
+      if constexpr (ng > 0) {
+        constexpr int every = 16 / (4 * (ng > 0 ? ng : 1));
+        if (q % every == 0) load(4 * g0 + q / every, dbuf, k0);
+      }
+      __builtin_amdgcn_sched_barrier(0);
     }
   };
-  auto mma = [&]() __attribute__((always_inline)) {
-#pragma unroll
-    for (int k2 = 0; k2 < 2; ++k2)
-#pragma unroll
-      for (int i = 0; i < FM; ++i)
-#pragma unroll
-        for (int j = 0; j < FN; ++j) acc[i][j] = mfma_32x32x16(fa[k2][i], fb[k2][j], acc[i][j]);
-  };
-
-  // A phase boundary: the workgroup barrier, fenced so that the compiler
-  // cannot move MFMAs (which touch no memory) across it.
-  auto phase = []() __attribute__((always_inline)) {
-    __builtin_amdgcn_sched_barrier(0);
-    __syncthreads();
-    __builtin_amdgcn_sched_barrier(0);
+  using T = std::true_type;
+  using F = std::false_type;
+  using N0 = std::integral_constant<int, 0>;
+  using N2 = std::integral_constant<int, 2>;
+  // substeps 1-3 of the step in buffer buf (+ the second half of the next
+  // step's loads, if any)
+  auto rest = [&](int buf, bool ld, int k0) __attribute__((always_inline)) {
+    if (ld)
+      phase(T{}, T{}, N2{}, 0, buf, 1, 1, 2, buf ^ 1, k0);
+    else
+      phase(T{}, T{}, N0{}, 0, buf, 1, 1, 0, 0, 0);
+    phase(T{}, T{}, N0{}, 1, buf, 2, 0, 0, 0, 0);
+    phase(T{}, T{}, N0{}, 0, buf, 3, 1, 0, 0, 0);
   };
 
   const int ksteps = a.K / BK;
-  // prologue: K step 0 in LDS, K step 1 in the stage registers
-  fetch(0, 0);
-  fetch(0, 1);
-  if constexpr (Epi::kInit) epi.template init<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
-  stash(0, 0);
-  stash(0, 1);
-  if (ksteps > 1) {
-    fetch(BK, 0);
-    fetch(BK, 1);
-  }
-  phase();
-  if (grp == 1) phase();  // group 1 runs one phase behind
-
-  for (int ks = 0; ks < ksteps; ++ks) {
-    const int cur = ks & 1;
 #pragma unroll
-    for (int h = 0; h < 2; ++h) {
-      read_frags(cur, h);
-      if (ks + 1 < ksteps) {
-        stash(cur ^ 1, h);
-        if (ks + 2 < ksteps) fetch((ks + 2) * BK, h);
-      }
-      phase();
-      mma();
-      phase();
+  for (int q = 0; q < 16; ++q) load(q, 0, 0);
+  wait_loads_barrier();
+  if (ksteps > 1) {
+    phase(F{}, T{}, N2{}, 1, 0, 0, 0, 0, 1, BK);
+    rest(0, true, BK);
+    wait_loads_barrier();
+    for (int k = 1; k + 1 < ksteps; ++k) {
+      const int buf = k & 1;
+      phase(T{}, T{}, N2{}, 1, buf, 0, 0, 0, buf ^ 1, (k + 1) * BK);
+      rest(buf, true, (k + 1) * BK);
+      wait_loads_barrier();
     }
+    phase(T{}, T{}, N0{}, 1, (ksteps - 1) & 1, 0, 0, 0, 0, 0);
+    rest((ksteps - 1) & 1, false, 0);
+  } else {
+    phase(F{}, T{}, N0{}, 1, 0, 0, 0, 0, 0, 0);
+    rest(0, false, 0);
   }
-  if (grp == 0) phase();  // match group 1's extra barrier
+  phase(T{}, F{}, N0{}, 1, 0, 0, 0, 0, 0, 0);
 
-  epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane);
+  // every wave is past its last LDS read: the tile buffers become the
+  // epilogue's staging area, one 64 KiB half per pair of waves
+  asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
+  char* half = wave < 2 ? (char*)&sA[0][0] : (char*)&sB[0][0];
+  epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane, half, wave & 1);
 }
-
-// 256 x 256 tiles, 8 waves as 4 (M) x 2 (N): 64 x 128 per wave, so a wave's
-// columns span whole 128-wide heads (RoPE pairs stay lane-local).
-constexpr int kBM = 256, kBN = 256, kWM = 4, kWN = 2;
 
 template <class Epi>
 hipError_t launch(GemmArgs a, const Epi& epi, hipStream_t s) {
@@ -376,9 +515,9 @@ hipError_t launch(GemmArgs a, const Epi& epi, hipStream_t s) {
   // operand offsets are 32-bit buffer offsets: W and a 256-row A panel must
   // stay below 2 GiB, and K must be whole 64-wide steps
   const long w_bytes = (long)epi.w_rows() * a.ldw * 2, a_panel = 256L * a.lda * 2;
-  if (w_bytes >= (1L << 31) || a_panel >= (1L << 31) || a.K % BK) return hipErrorInvalidValue;
+  if (w_bytes >= (1L << 31) || a_panel >= (1L << 31) || a.K % BK || a.K <= 0) return hipErrorInvalidValue;
   a.w_bytes = (int)w_bytes;
-  hipLaunchKernelGGL((gemm_pp_kernel<Epi>), dim3(tiles), dim3(512), 0, s, a, epi);
+  hipLaunchKernelGGL((gemm_kernel<Epi>), dim3(tiles), dim3(256), 0, s, a, epi);
   return hipGetLastError();
 }
 
