@@ -11,9 +11,9 @@
 // Tiling: a workgroup of 4 waves (one per SIMD) computes a 256 x 256 tile,
 // each wave a 128 x 128 sub-tile of 4 x 4 32x32 blocks
 // (v_mfma_f32_32x32x16_bf16, accumulators in the 256 accumulation registers).
-// K advances in steps of 64 through two LDS tile buffers; operand tiles are
-// loaded straight into LDS (buffer loads with the LDS bit), so no register
-// staging is needed.  LDS rows are 128 bytes (64 bf16) with an XOR-swizzled
+// K advances in steps of 64 through LDS rings of three A tiles and two W
+// tiles (160 KiB); operand tiles are loaded straight into LDS (buffer loads
+// with the LDS bit), so no register staging is needed.  LDS rows are 128 bytes (64 bf16) with an XOR-swizzled
 // 16-byte chunk index (see swz), conflict-free for the fragment reads.  After
 // the K loop the tile buffers become the epilogue's staging area: every
 // epilogue writes its outputs as whole 16-byte row chunks.
@@ -343,34 +343,40 @@ __device__ __forceinline__ void load_lds16(i32x4 rsrc, uint32_t voff, uint32_t s
 }
 #pragma clang diagnostic pop
 
-// Waits for this wave's loads into LDS and its LDS reads, then the workgroup
-// barrier, in one statement so that no LDS access moves across it.
+// Wait for this wave's LDS reads and for all (or all but the 8 newest) of its
+// loads into LDS, then the workgroup barrier, in one statement so that no LDS
+// access moves across it.
 __device__ __forceinline__ void wait_loads_barrier() {
   asm volatile("s_waitcnt vmcnt(0) lgkmcnt(0)\n\ts_barrier" ::: "memory");
 }
+__device__ __forceinline__ void wait_loads_but8_barrier() {
+  asm volatile("s_waitcnt vmcnt(8) lgkmcnt(0)\n\ts_barrier" ::: "memory");
+}
 
 // ---------------------------------------------------------------- kernel
-// K step k (64 of K) uses LDS buffer k % 2 and is four substeps of 16 of K;
-// a "phase" is the 16 MFMAs of one substep.  Each K step starts right after
-// the barrier that published its tiles: its first phase runs the last substep
-// of step k - 1 (fragments already in registers) beside the first fragment
-// reads of step k, and the loads of step k + 1 go to the other buffer, whose
-// last reads (step k - 1) all happened before that barrier.  Substeps 0-2 of
-// step k each run beside the next substep's fragment reads; the barrier that
-// closes the step follows once this wave's loads have landed.  The 16 loads of
-// a K step (8 A, 8 W per wave) are spread one per two MFMAs over the first two
-// phases: issued in one phase they stall the wave (the address unit takes them
-// slower than the phase issues them); issued later they have too little time
-// to land.  Every phase is a fixed sequence: sched_barrier keeps the compiler
-// from regrouping it.
+// K step k (64 of K) reads A buffer k % 3 and W buffer k % 2 and is four
+// substeps of 16 of K; a "phase" is the 16 MFMAs of one substep.  Each K step
+// starts right after the barrier that published its tiles.  Its first phase
+// runs the last substep of step k - 1 (fragments already in registers) beside
+// the first fragment reads of step k; each later phase runs beside the next
+// substep's fragment reads.  The 16 loads of a wave per K step are spread one
+// per four MFMAs over all four phases: the W tile of step k + 1 in the first
+// two (its buffer was last read in step k - 1), the A tile of step k + 2 in the
+// last two (its buffer, (k - 1) % 3, too).  So the A loads have more than a K
+// step to land, and no phase issues more than 16 loads per CU: the CU's
+// address unit takes about 13 cycles per 16-byte load, and a burst of 64 (all
+// of a K step's loads in one or two phases) stalls the waves that issue them.
+// The barrier closing step k waits for all but this wave's 8 newest loads
+// (step k + 2's A tile).  Every phase is a fixed sequence: sched_barrier keeps
+// the compiler from regrouping it.
 template <class Epi>
 __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
   constexpr int BM = 256, BN = 256, TM = 128, TN = 128, FM = 4, FN = 4;
   constexpr uint32_t kNoRow = 0x80000000u;  // offset past every buffer range
   static_assert(2 * Epi::kSlotBytes(TN, TM) <= BM * BK * 2 * 2, "epilogue staging exceeds half the tile buffers");
 
-  __shared__ __attribute__((aligned(1024))) bf16 sA[2][BM * BK];
-  __shared__ __attribute__((aligned(1024))) bf16 sB[2][BN * BK];
+  __shared__ __attribute__((aligned(1024))) bf16 sA[3][BM * BK];  // A ring: K step k in k % 3
+  __shared__ __attribute__((aligned(1024))) bf16 sB[2][BN * BK];  // W ring: K step k in k % 2
 
   const int tid = threadIdx.x, lane = tid & 63;
   const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -421,6 +427,7 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
   const uint32_t ldsA = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16*)&sA[0][0];
   const uint32_t ldsB = (uint32_t)(uintptr_t)(__attribute__((address_space(3))) bf16*)&sB[0][0];
   constexpr uint32_t kBuf = BM * BK * 2;  // bytes of one tile buffer
+  // q < 8: A load into A buffer buf; q >= 8: W load into W buffer buf
   auto load = [&](int q, int buf, int k0) __attribute__((always_inline)) {
     const uint32_t lds = (q < 8 ? ldsA : ldsB) + buf * kBuf + (8 * wave + (q & 4)) * 1024;
     load_lds16(q < 8 ? ra : rw, voff[q], __builtin_amdgcn_readfirstlane(k0 * 2),
@@ -433,76 +440,85 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
 #pragma unroll
     for (int j = 0; j < FN; ++j) acc[i][j] = zero16();
 
-  // fragment f < 4: A block f, f >= 4: W block f - 4, of substep s
+  // fragment f < 4: A block f, f >= 4: W block f - 4, of substep s of K step k
   bf16x8 fr[2][8];
-  auto read_frag = [&](int buf, int s, int set, int f) __attribute__((always_inline)) {
+  auto read_frag = [&](int k, int s, int set, int f) __attribute__((always_inline)) {
     const int kci = s * 2 + (lane >> 5);
     if (f < 4)
-      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sA[buf][swz(wm * TM + f * 32 + (lane & 31), kci)]);
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sA[k % 3][swz(wm * TM + f * 32 + (lane & 31), kci)]);
     else
-      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sB[buf][swz(wn * TN + (f - 4) * 32 + (lane & 31), kci)]);
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sB[k & 1][swz(wn * TN + (f - 4) * 32 + (lane & 31), kci)]);
   };
   // reads in the order the next phase's MFMAs need them
   constexpr int kReadOrder[8] = {0, 4, 5, 6, 7, 1, 2, 3};
   // One phase: the 16 MFMAs of the fragments in set mset (if MMA), the 8
-  // fragment reads of substep rs of buffer rbuf into set rset (if RD), and NG
-  // load groups (4 loads each), starting at group g0, of the K step at k0 into
-  // buffer dbuf, one load per 16 / (4 NG) MFMAs.
-  auto phase = [&](auto MMA, auto RD, auto NG, int mset, int rbuf, int rs, int rset, int g0, int dbuf, int k0)
+  // fragment reads of substep rs of K step rk into set rset (if RD), and (if
+  // LD) 4 loads q0 .. q0+3 of the K step at k0 into buffer dbuf, one per 4 MFMAs.
+  auto phase = [&](auto MMA, auto RD, auto LD, int mset, int rk, int rs, int rset, int q0, int dbuf, int k0)
       __attribute__((always_inline)) {
-    constexpr int ng = decltype(NG)::value;
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       if constexpr (decltype(MMA)::value)
         acc[q >> 2][q & 3] = mfma_32x32x16(fr[mset][q >> 2], fr[mset][4 + (q & 3)], acc[q >> 2][q & 3]);
       if constexpr (decltype(RD)::value)
-        if ((q & 1) == 0) read_frag(rbuf, rs, rset, kReadOrder[q >> 1]);
-      if constexpr (ng > 0) {
-        constexpr int every = 16 / (4 * (ng > 0 ? ng : 1));
-        if (q % every == 0) load(4 * g0 + q / every, dbuf, k0);
-      }
+        if ((q & 1) == 0) read_frag(rk, rs, rset, kReadOrder[q >> 1]);
+      if constexpr (decltype(LD)::value)
+        if ((q & 3) == 0) load(q0 + (q >> 2), dbuf, k0);
       __builtin_amdgcn_sched_barrier(0);
     }
   };
   using T = std::true_type;
   using F = std::false_type;
-  using N0 = std::integral_constant<int, 0>;
-  using N2 = std::integral_constant<int, 2>;
-  // substeps 1-3 of the step in buffer buf (+ the second half of the next
-  // step's loads, if any)
-  auto rest = [&](int buf, bool ld, int k0) __attribute__((always_inline)) {
-    if (ld)
-      phase(T{}, T{}, N2{}, 0, buf, 1, 1, 2, buf ^ 1, k0);
-    else
-      phase(T{}, T{}, N0{}, 0, buf, 1, 1, 0, 0, 0);
-    phase(T{}, T{}, N0{}, 1, buf, 2, 0, 0, 0, 0);
-    phase(T{}, T{}, N0{}, 0, buf, 3, 1, 0, 0, 0);
-  };
 
+  // K step k:
+  //   phase 0: MFMAs of step k-1 substep 3, reads of step k substep 0,
+  //            W loads 0-3 of step k+1
+  //   phase 1: substep 0, reads of substep 1, W loads 4-7 of step k+1
+  //   phase 2: substep 1, reads of substep 2, A loads 0-3 of step k+2
+  //   phase 3: substep 2, reads of substep 3, A loads 4-7 of step k+2
+  //   barrier: step k+1's W (this step) and A (previous step) have landed.
+  // The prologue loads A and W of step 0 and A of step 1.
   const int ksteps = a.K / BK;
 #pragma unroll
-  for (int q = 0; q < 16; ++q) load(q, 0, 0);
-  wait_loads_barrier();
+  for (int q = 0; q < 16; ++q) load(q, 0, 0);                       // A(0), W(0)
   if (ksteps > 1) {
-    phase(F{}, T{}, N2{}, 1, 0, 0, 0, 0, 1, BK);
-    rest(0, true, BK);
-    wait_loads_barrier();
-    for (int k = 1; k + 1 < ksteps; ++k) {
-      const int buf = k & 1;
-      phase(T{}, T{}, N2{}, 1, buf, 0, 0, 0, buf ^ 1, (k + 1) * BK);
-      rest(buf, true, (k + 1) * BK);
-      wait_loads_barrier();
-    }
-    phase(T{}, T{}, N0{}, 1, (ksteps - 1) & 1, 0, 0, 0, 0, 0);
-    rest((ksteps - 1) & 1, false, 0);
+#pragma unroll
+    for (int q = 0; q < 8; ++q) load(q, 1, BK);                      // A(1)
+    wait_loads_but8_barrier();
   } else {
-    phase(F{}, T{}, N0{}, 1, 0, 0, 0, 0, 0, 0);
-    rest(0, false, 0);
+    wait_loads_barrier();
   }
-  phase(T{}, F{}, N0{}, 1, 0, 0, 0, 0, 0, 0);
+  auto body = [&](int k, auto FIRST, auto LDW, auto LDA) __attribute__((always_inline)) {
+    const int k1 = (k + 1) * BK, k2 = (k + 2) * BK;
+    phase(std::integral_constant<bool, !decltype(FIRST)::value>{}, T{}, LDW, 1, k, 0, 0, 8, (k + 1) & 1, k1);
+    phase(T{}, T{}, LDW, 0, k, 1, 1, 12, (k + 1) & 1, k1);
+    phase(T{}, T{}, LDA, 1, k, 2, 0, 0, (k + 2) % 3, k2);
+    phase(T{}, T{}, LDA, 0, k, 3, 1, 4, (k + 2) % 3, k2);
+  };
+  using B1 = std::true_type;
+  using B0 = std::false_type;
+  if (ksteps >= 3) {
+    body(0, B1{}, T{}, T{});
+    wait_loads_but8_barrier();
+    for (int k = 1; k + 2 < ksteps; ++k) {
+      body(k, B0{}, T{}, T{});
+      wait_loads_but8_barrier();
+    }
+    body(ksteps - 2, B0{}, T{}, F{});
+    wait_loads_barrier();
+    body(ksteps - 1, B0{}, F{}, F{});
+  } else if (ksteps == 2) {
+    body(0, B1{}, T{}, F{});
+    wait_loads_barrier();
+    body(1, B0{}, F{}, F{});
+  } else {
+    body(0, B1{}, F{}, F{});
+  }
+  phase(T{}, F{}, F{}, 1, 0, 0, 0, 0, 0, 0);
 
   // every wave is past its last LDS read: the tile buffers become the
-  // epilogue's staging area, one 64 KiB half per pair of waves
+  // epilogue's staging area, 64 KiB (of the A ring, or the W ring) per pair of
+  // waves
   asm volatile("s_waitcnt lgkmcnt(0)\n\ts_barrier" ::: "memory");
   char* half = wave < 2 ? (char*)&sA[0][0] : (char*)&sB[0][0];
   epi.template apply<BN, TN, FM, FN>(acc, a.M, tn, m0 + wm * TM, wn, lane, half, wave & 1);
