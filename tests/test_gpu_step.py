@@ -23,6 +23,10 @@ SMALL = [
     # Dream-like grouping (7 query heads per KV head), tiny suffix
     dict(cfg=synth.model_config(n_layers=2, hidden=896, n_heads=7, n_kv_heads=1, head_dim=128, ffn=640),
          m=70, n_s=1, B=4, seed=13),
+    # the GEMMs' shortest K loops: K = 64 (one K step: QKV, O, gate/up) and
+    # K = 192 (three: down); output tiles mostly empty (N = 64, 192)
+    dict(cfg=synth.model_config(n_layers=2, hidden=64, n_heads=1, n_kv_heads=1, head_dim=64, ffn=192),
+         m=77, n_s=33, B=3, seed=14),
 ]
 
 
@@ -43,7 +47,7 @@ class Setup:
         self.cache64 = OT.populate(to_f64(self.xp), self.w64, cfg, cfg["n_layers"])
 
 
-@pytest.fixture(scope="module", params=range(len(SMALL)), ids=["gqa64", "mha128", "g7n1"])
+@pytest.fixture(scope="module", params=range(len(SMALL)), ids=["gqa64", "mha128", "g7n1", "k64"])
 def setup(request):
     s = Setup(SMALL[request.param])
     yield s
