@@ -252,7 +252,9 @@ enum {
  * each over a prefix of m tokens at reuse depth d.  Layout: for each deep
  * layer l = d..L-1, K then V, each [B][Hkv][m + n_s][dh] bf16 (post-RoPE, the
  * refresh step's K/V of every row of the request; reuse steps read rows
- * 0..m-1).  Returns 0 for invalid arguments and for d = L (no deep layers). */
+ * 0..m-1), then a 256-byte header that the refresh step writes (its tag, see
+ * bc_step_forward_deep).  Returns 0 for invalid arguments and for d = L (no
+ * deep layers). */
 size_t bc_deep_store_bytes(const bc_model* model, int m, int B, int n_s, int d);
 
 /* Byte offset inside a deep store of element (layer, part, req, head, pos,
@@ -281,8 +283,12 @@ bc_status bc_deep_store_reset(bc_model* model, const void* deep_store);
  *        carry the tag of a refresh step with the same key, m, B, n_s and d
  *        (else BC_E_STATE); request b of this call must be request b of that
  *        refresh.  The library keeps the tag on the host, keyed by the store's
- *        address: it cannot tell whether the memory was overwritten since
- *        (bc_deep_store_reset drops the tag).
+ *        address (bc_deep_store_reset drops it).  The refresh also writes the
+ *        tag, with a number unique to that refresh, into the store's last 256
+ *        bytes; the reuse step compares them on the device and, if they
+ *        differ (the memory was overwritten since), writes NaN to every
+ *        element of `out` (no error code: the check runs on the stream).
+ *        Memory overwritten only inside the K/V blocks goes undetected.
  *   At d = L there are no deep layers: both modes equal bc_step_forward and
  *   deep_store is ignored (may be NULL).
  *   deep_store  device, >= bc_deep_store_bytes(model, m, B, n_s, d) bytes,

@@ -153,4 +153,42 @@ hipError_t rope_table(float* cos_t, float* sin_t, int n_pos, int dh, double thet
   return hipGetLastError();
 }
 
+// ---------------------------------------------------------------- deep-store header
+namespace {
+__global__ void __launch_bounds__(64) deep_header_write_kernel(uint64_t* hdr, DeepHeader h) {
+  const int t = threadIdx.x;
+  if (t < 8) hdr[t] = h.w[t];
+}
+
+// Every workgroup compares the header; on a mismatch the grid fills out.
+__global__ void __launch_bounds__(256) deep_header_check_kernel(const uint64_t* hdr, DeepHeader h,
+                                                                float* out, long n) {
+  __shared__ int bad;
+  if (threadIdx.x == 0) {
+    int b = 0;
+#pragma unroll
+    for (int i = 0; i < 8; ++i) b |= hdr[i] != h.w[i];
+    bad = b;
+  }
+  __syncthreads();
+  if (!bad) return;
+  const float nan = __builtin_nanf("");
+  for (long i = (long)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += (long)gridDim.x * blockDim.x)
+    out[i] = nan;
+}
+}  // namespace
+
+hipError_t deep_header_write(uint64_t* hdr, const DeepHeader& h, hipStream_t s) {
+  hipLaunchKernelGGL(deep_header_write_kernel, dim3(1), dim3(64), 0, s, hdr, h);
+  return hipGetLastError();
+}
+
+hipError_t deep_header_check(const uint64_t* hdr, const DeepHeader& h, float* out, long n,
+                             hipStream_t s) {
+  const long blocks = (n + 1023) / 1024;
+  const int grid = (int)(blocks < 1 ? 1 : blocks > 1024 ? 1024 : blocks);
+  hipLaunchKernelGGL(deep_header_check_kernel, dim3(grid), dim3(256), 0, s, hdr, h, out, n);
+  return hipGetLastError();
+}
+
 }  // namespace bc

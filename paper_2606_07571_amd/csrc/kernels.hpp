@@ -84,6 +84,17 @@ hipError_t cosine_scratch(double** ptr);
 hipError_t kv_cosine(const CosView& v, double* partial, double* out, long out_req, long out_layer,
                      hipStream_t s);
 
+// ----- deep-store header: 8 words a refresh step writes after the store's
+// K/V blocks and a reuse step checks (see runtime.cpp)
+struct DeepHeader {
+  uint64_t w[8];
+};
+// hdr[0..8) = h.w (device, 8-byte aligned)
+hipError_t deep_header_write(uint64_t* hdr, const DeepHeader& h, hipStream_t s);
+// if hdr[0..8) differs from h.w anywhere, out[0..n) = NaN; otherwise nothing
+hipError_t deep_header_check(const uint64_t* hdr, const DeepHeader& h, float* out, long n,
+                             hipStream_t s);
+
 // ----- elementwise / normalisation
 // out[r, :] = bf16(x[r, :] / sqrt(mean(x[r, :]^2) + eps) * gain)
 hipError_t rmsnorm(const float* x, const void* gain, void* out, int rows, int h, float eps,

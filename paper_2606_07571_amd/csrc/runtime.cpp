@@ -15,6 +15,7 @@
 #include <cstdint>
 #include <new>
 #include <string>
+#include <atomic>
 #include <mutex>
 #include <unordered_map>
 #include <unordered_set>
@@ -37,11 +38,26 @@ struct Profiler {
 };
 
 // What the last refresh step wrote into a deep store (keyed by its address):
-// a reuse step must match it.
+// a reuse step must match it.  `nonce` is unique to that refresh (process-wide
+// counter); the refresh also writes the tag into the store's header, and a
+// reuse step compares the two on the device (deep_header_words).
 struct DeepTag {
   uint64_t key;
   int m, B, n_s, d;
+  uint64_t nonce;
 };
+static std::atomic<uint64_t> g_deep_nonce{1};
+constexpr uint64_t kDeepMagic = 0x3130504545444342ull;  // "BCDEEP01"
+static bc::DeepHeader deep_header_words(const DeepTag& t) {
+  bc::DeepHeader h{};
+  h.w[0] = kDeepMagic;
+  h.w[1] = t.key;
+  h.w[2] = (uint64_t)(uint32_t)t.m | (uint64_t)(uint32_t)t.B << 32;
+  h.w[3] = (uint64_t)(uint32_t)t.n_s | (uint64_t)(uint32_t)t.d << 32;
+  h.w[4] = t.nonce;
+  h.w[5] = ~(t.key ^ t.nonce);
+  return h;
+}
 
 struct bc_model {
   bc_model_config cfg;
@@ -161,9 +177,12 @@ EntryLayout entry_layout(const bc_model_config& c, int m, int Lc) {
 
 // Deep store of a batch: for each deep layer l in [d, L), K then V, each
 // [B][Hkv][N][dh] bf16 with N = m + n_s (the refresh step's K/V of every row;
-// reuse steps read rows 0..m-1).  Every block is a multiple of 256 bytes.
+// reuse steps read rows 0..m-1), then a 256-byte header (the refresh's tag).
+// Every block is a multiple of 256 bytes.
+constexpr size_t kDeepHeaderBytes = 256;
 struct DeepLayout {
-  size_t part = 0;  // bytes of one layer's K or V block
+  size_t part = 0;    // bytes of one layer's K or V block
+  size_t header = 0;  // offset of the header
   size_t total = 0;
   long sb = 0, sh = 0;  // request and head strides (elements)
 };
@@ -174,7 +193,9 @@ DeepLayout deep_layout(const bc_model_config& c, int m, int B, int n_s, int d) {
   dl.sh = N * c.head_dim;
   dl.sb = (long)c.n_kv_heads * dl.sh;
   dl.part = (size_t)B * dl.sb * 2;
-  dl.total = (size_t)(c.n_layers - d) * 2 * dl.part;
+  if (d >= c.n_layers) return dl;  // no deep layers: no store
+  dl.header = align_up((size_t)(c.n_layers - d) * 2 * dl.part);
+  dl.total = dl.header + kDeepHeaderBytes;
   return dl;
 }
 
@@ -403,11 +424,13 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
     if (store_bytes < dl.total) return fail(BC_E_INVALID, "deep store %zu < required %zu", store_bytes, dl.total);
     if ((uintptr_t)store % kAlign) return fail(BC_E_INVALID, "deep store must be 256-byte aligned");
   }
+  DeepTag reuse_tag{};
   if (use_store && mode == BC_DEEP_REUSE) {
     auto it = model->deep_tags.find((uintptr_t)store);
     if (it == model->deep_tags.end())
       return fail(BC_E_STATE, "no refresh step has written this deep store");
     const DeepTag& tg = it->second;
+    reuse_tag = tg;
     if (tg.key != key0 || tg.m != m0 || tg.B != B || tg.n_s != n_s || tg.d != d)
       return fail(BC_E_STATE,
                   "deep store was refreshed for key %016llx m=%d B=%d n_s=%d d=%d, not key %016llx m=%d B=%ld n_s=%d d=%d",
@@ -489,7 +512,18 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
       row0 += (long)cnt * (m + n_s);
       first += cnt;
     }
-    if (use_store) model->deep_tags[(uintptr_t)store] = DeepTag{key0, m0, (int)B, n_s, d};
+    if (use_store) {
+      const DeepTag tg{key0, m0, (int)B, n_s, d, g_deep_nonce.fetch_add(1)};
+      BC_LAUNCH(model, BC_K_OTHER, s,
+                bc::deep_header_write((uint64_t*)(st_mem + dl.header), deep_header_words(tg), s));
+      model->deep_tags[(uintptr_t)store] = tg;
+    }
+  } else if (use_store) {
+    // a reuse step: if the store's header is not the tag of the refresh the
+    // host recorded (the memory was overwritten since), every output is NaN
+    BC_LAUNCH(model, BC_K_OTHER, s,
+              bc::deep_header_check((const uint64_t*)(st_mem + dl.header), deep_header_words(reuse_tag),
+                                    out, B * n_s * h, s));
   }
   return ok();
 }

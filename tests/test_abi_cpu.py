@@ -189,7 +189,8 @@ def test_deep_store_layout_offsets():
     N = m + n_s
     for d in range(nl + 1):
         part = B * Hkv * N * dh * 2
-        assert L.bc_deep_store_bytes(h, m, B, n_s, d) == (nl - d) * 2 * part
+        # the K/V blocks, then a 256-byte header (the refresh's tag) when there are deep layers
+        assert L.bc_deep_store_bytes(h, m, B, n_s, d) == ((nl - d) * 2 * part + 256 if d < nl else 0)
         assert part % 256 == 0
         for (layer, pt, req, head, pos, dim) in [(d, 0, 0, 0, 0, 0), (nl - 1, 1, B - 1, Hkv - 1, N - 1, dh - 1),
                                                  (d, 1, 1, 0, m, 3)]:
@@ -208,9 +209,9 @@ def test_deep_store_layout_offsets():
     assert L.bc_deep_store_offset(h, m, B, n_s, d, 1, 0, 0, 0, N, 0) == bad      # pos >= N
     assert L.bc_deep_store_bytes(h, m, B, n_s, 4) == 0
     assert L.bc_deep_store_bytes(h, 0, B, n_s, 1) == 0
-    # the last element ends the store
+    # the last element ends the K/V blocks; the 256-byte header follows
     last = L.bc_deep_store_offset(h, m, B, n_s, 0, nl - 1, 1, B - 1, Hkv - 1, N - 1, dh - 1)
-    assert last + 2 == L.bc_deep_store_bytes(h, m, B, n_s, 0)
+    assert last + 2 + 256 == L.bc_deep_store_bytes(h, m, B, n_s, 0)
     L.bc_model_destroy(h)
 
 

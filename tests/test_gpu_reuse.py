@@ -153,7 +153,9 @@ def test_refresh_writes_deep_prefix_kv(seq):
     s.model.step(s.key, s.xsteps[0].cuda(), d, deep="refresh", deep_store=store)
     torch.cuda.synchronize()
     assert s.model.deep_store_offset(m, B, n_s, d, d, 0, 0, 0, 0, 0) == 0
-    kv = store.view(torch.bfloat16).view(L - d, 2, B, Hkv, N, dh).cpu().double().numpy()
+    body = (L - d) * 2 * B * Hkv * N * dh * 2            # K/V blocks; the 256-byte header follows
+    assert store.numel() == body + 256
+    kv = store[:body].view(torch.bfloat16).view(L - d, 2, B, Hkv, N, dh).cpu().double().numpy()
     x64 = to_f64(s.xsteps[0])
     for b in range(B):
         rec = {}
@@ -220,3 +222,47 @@ def test_reuse_store_tag_checks(seq):
     with pytest.raises(bc.BiCacheError) as e:
         s.model.step(s.key, xs, 0, deep="reuse", deep_store=store)
     assert e.value.status == -5
+
+
+def test_reuse_of_an_overwritten_store_gives_nan(seq):
+    """The host tag of a store is keyed by its address; the refresh also writes
+    it, with a number unique to that refresh, into the store's last 256 bytes,
+    and a reuse step checks it on the device.  A store whose memory was put to
+    other use (here: zeroed) without bc_deep_store_reset passes the host check,
+    and the reuse step then writes NaN to every output instead of results from
+    stale K/V.  A refresh restores it; a refresh into another store at the same
+    parameters does not make the first store's header valid for the second."""
+    s = seq
+    B, n_s = s.spec["B"], s.spec["n_s"]
+    xs = s.xsteps[1].cuda()
+    d = 1
+    store = s.model.new_deep_store(s.key, B, n_s, d)
+    ref = s.model.step(s.key, xs, d, deep="refresh", deep_store=store)
+    good = s.model.step(s.key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.isfinite(good).all()
+    say("reuse of an overwritten store")
+    store.zero_()                                          # memory put to other use
+    bad = s.model.step(s.key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.isnan(bad).all()
+    # only the header overwritten: also refused
+    s.model.step(s.key, xs, d, deep="refresh", deep_store=store)
+    store[-256:].fill_(7)
+    bad = s.model.step(s.key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.isnan(bad).all()
+    # a refresh restores it, bit for bit the same reuse output as before
+    s.model.step(s.key, xs, d, deep="refresh", deep_store=store)
+    again = s.model.step(s.key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.equal(again, good)
+    # a second store refreshed with the same parameters: copying its bytes over
+    # the first carries its own refresh number, which the first's tag lacks
+    other = s.model.new_deep_store(s.key, B, n_s, d)
+    s.model.step(s.key, xs, d, deep="refresh", deep_store=other)
+    store.copy_(other)
+    bad = s.model.step(s.key, xs, d, deep="reuse", deep_store=store)
+    torch.cuda.synchronize()
+    assert torch.isnan(bad).all()
+    assert torch.isfinite(ref).all()
