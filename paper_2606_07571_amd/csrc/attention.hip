@@ -463,28 +463,57 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   if (u < n_tiles) step(u, T_{}, S1{}, p, sc, fr);
   pv(n_tiles - 1, p);
 
+  // Output.  A lane holds dims nb*32 + 8j + 4*half + {0..3} of its query row,
+  // so direct stores would write 8 or 16 bytes into each of 32 rows per
+  // instruction.  Instead each wave writes its 32 rows into a region of its
+  // own in two ring slots no longer in use (every slot but the last tile's,
+  // which other waves may still be reading: the final barrier has passed),
+  // and reads them back as runs of whole rows (256 bytes of a row per pass
+  // of DPP dims at dh = 128, 128 at dh = 64), 16 bytes per lane, so that a
+  // store instruction writes 4 (or 8) row runs.  Nothing else touches the
+  // region: no barrier.
   const float l0 = __shfl(lacc[0], c & 15, 64), l1 = __shfl(lacc[1], c & 15, 64);
-  if (!row_ok) return;
   const float inv = 1.f / (c < 16 ? l0 : l1);
-  if constexpr (OUT_F32) {
-    float* op = (float*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
+  {
+    typedef std::conditional_t<OUT_F32, float, bf16> OT;
+    constexpr int ES = sizeof(OT);
+    constexpr int RMAX = DH >= 128 ? 256 : 128;          // row bytes per pass at most
+    constexpr int DPP = DH * ES > RMAX ? RMAX / ES : DH;  // dims per pass
+    constexpr int RBY = DPP * ES;                        // bytes of a row per pass
+    constexpr int RST = RBY + 16;                        // LDS row stride (bytes)
+    constexpr int LPR = RBY / 16;                        // lanes per row on the way out
+    constexpr int RPI = 64 / LPR;                        // rows per store instruction
+    static_assert(NW * QR * RST <= 2 * SLOT * 2, "staging must fit in two slots");
+    const int busy = (n_tiles - 1) % NBUF;
+    const int s0 = busy >= 2 ? 0 : busy + 1;             // first of two free, adjacent slots
+    char* reg = reinterpret_cast<char*>(smem + s0 * SLOT) + wave * (QR * RST);
+    const int nrow = active ? a.n_s - i0 : 0;            // valid rows of this wave's chunk
+    OT* ob = (OT*)a.out + b * a.o_sb + hq * a.o_sh + (long)i0 * a.o_sr;
 #pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
+    for (int q = 0; q < DH / DPP; ++q) {
 #pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        f32x4 v = {o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv, o[nb][4 * j + 2] * inv, o[nb][4 * j + 3] * inv};
-        *reinterpret_cast<f32x4*>(op + nb * 32 + 8 * j + 4 * half) = v;
+      for (int nb = q * DPP / 32; nb < (q + 1) * DPP / 32; ++nb)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          char* d = reg + c * RST + (nb * 32 + 8 * j + 4 * half - q * DPP) * ES;
+          if constexpr (OUT_F32) {
+            const f32x4 v = {o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv, o[nb][4 * j + 2] * inv,
+                             o[nb][4 * j + 3] * inv};
+            *reinterpret_cast<f32x4*>(d) = v;
+          } else {
+            const u32x2 v = {pack_bf16x2(o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv),
+                             pack_bf16x2(o[nb][4 * j + 2] * inv, o[nb][4 * j + 3] * inv)};
+            *reinterpret_cast<u32x2*>(d) = v;
+          }
+        }
+#pragma unroll
+      for (int k = 0; k < QR / RPI; ++k) {
+        const int row = k * RPI + lane / LPR, ch = lane % LPR;
+        const u32x4 v = *reinterpret_cast<const u32x4*>(reg + row * RST + ch * 16);
+        if (row < nrow)
+          *reinterpret_cast<u32x4*>(ob + (long)row * a.o_sr + q * DPP + ch * (16 / ES)) = v;
       }
-  } else {
-    bf16* op = (bf16*)a.out + b * a.o_sb + hq * a.o_sh + (long)qrow * a.o_sr;
-#pragma unroll
-    for (int nb = 0; nb < NB; ++nb)
-#pragma unroll
-      for (int j = 0; j < 4; ++j) {
-        u32x2 v = {pack_bf16x2(o[nb][4 * j] * inv, o[nb][4 * j + 1] * inv),
-                   pack_bf16x2(o[nb][4 * j + 2] * inv, o[nb][4 * j + 3] * inv)};
-        *reinterpret_cast<u32x2*>(op + nb * 32 + 8 * j + 4 * half) = v;
-      }
+    }
   }
 }
 
