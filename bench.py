@@ -41,11 +41,17 @@ def step_flops(cfg, B, m, n_s, d):
     attention 4*n_q*n_k*dh per (request, head), no causal halving."""
     h, F, L = cfg["hidden"], cfg["ffn"], cfg["n_layers"]
     Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
-    lin = 2 * (h * (Hq + 2 * Hkv) * dh + Hq * dh * h + 3 * h * F)
+    lin_qkv = 2 * h * (Hq + 2 * Hkv) * dh
+    lin = lin_qkv + 2 * (Hq * dh * h + 3 * h * F)
     N = m + n_s
     shallow = B * n_s * lin + 4 * B * Hq * n_s * N * dh
     deep = B * N * lin + 4 * B * Hq * N * N * dh
-    return d * shallow + (L - d) * deep
+    if d >= L:
+        return L * shallow
+    # the last layer's prefix rows only supply K/V: their attention, O
+    # projection and FFN outputs are never read, and are not computed
+    last = B * N * lin_qkv + B * n_s * (lin - lin_qkv) + 4 * B * Hq * n_s * N * dh
+    return d * shallow + (L - d - 1) * deep + last
 
 
 TRAFFIC_PROFILE = os.path.join(ROOT, "profiles", "gate_up_swiglu_c3_step_d8_traffic.md")
@@ -187,7 +193,8 @@ def main():
     value = B / (ms_per_step / 1e3)
 
     gu_ms, gu_n = prof["gate_up_swiglu"]
-    rows_per_step = d * B * n_s + (L - d) * B * (m + n_s)
+    # gate_up rows: suffix rows in the shallow layers and the last one, all rows between
+    rows_per_step = (L * B * n_s if d >= L else (d + 1) * B * n_s + (L - d - 1) * B * (m + n_s))
     gu_flops = gate_up_flops(cfg, rows_per_step) * args.steps
     gu_tflops = gu_flops / (gu_ms / 1e3) / 1e12
     roofline = {"bound": "mfma", "kernel": "gate_up_swiglu GEMM (bf16 MFMA)",
@@ -202,11 +209,13 @@ def main():
     breakdown = {k: round(v[0], 3) for k, v in prof.items()}
     # HBM-bound paths of the same step against the 8 TB/s peak, algorithmic
     # bytes only: RMSNorm reads the fp32 residual and writes the bf16 operand
-    # (two norms per layer over B*n_s rows below d, B*(m+n_s) rows from d on);
-    # the transition writes the full residual of every request and reads the
+    # (two norms per layer over B*n_s rows below d, B*(m+n_s) rows from d on,
+    # except the last layer's second norm, over the suffix rows only); the
+    # transition writes the full residual of every request and reads the
     # suffix rows and the cached prefix residual once
     h = cfg["hidden"]
-    norm_rows = 2 * (d * B * n_s + (L - d) * B * (m + n_s))
+    norm_rows = (2 * L * B * n_s if d >= L else
+                 2 * d * B * n_s + 2 * (L - d - 1) * B * (m + n_s) + B * (m + n_s) + B * n_s)
     norm_bytes = norm_rows * h * (4 + 2)
     trans_bytes = (B * (m + n_s) + B * n_s + m) * h * 4 if d < L else 0
     hbm = {}

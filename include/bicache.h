@@ -178,7 +178,10 @@ size_t bc_step_workspace_bytes(const bc_model* model, int m, int B, int n_s, int
  *   pos_base[l]  RoPE position of the first projected row of a request:
  *                m for l < d (suffix positions m..m+n_s-1), 0 otherwise
  *   reads_kv[l]  1 if layer l reads the cached KV$_l (l < d), else 0
- * and *reads_h (may be NULL) = the H$ layer re-entered at d (d < L), or -1. */
+ * and *reads_h (may be NULL) = the H$ layer re-entered at d (d < L), or -1.
+ * When d < L the last layer projects every row but runs attention, the O
+ * projection and the FFN over the B*n_s suffix rows only: the prefix rows'
+ * outputs of the last layer are never read, their K/V are. */
 bc_status bc_step_plan(const bc_model* model, int m, int B, int n_s, int d, int* rows,
                        int* pos_base, int* reads_kv, int* reads_h);
 

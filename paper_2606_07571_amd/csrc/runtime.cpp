@@ -337,6 +337,77 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
   return BC_OK;
 }
 
+// The last layer of a step whose deep layers run over every row.  Only the
+// suffix rows' outputs are ever read (the step returns them; nothing reads
+// the prefix rows' hidden states after the last layer), so once Q/K/V of
+// every row are projected (the suffix rows attend to the recomputed prefix
+// K/V, Eq. 5 first case) the suffix rows of the residual move to `out`, and
+// attention, the O projection and the FFN run over those rows alone.  Per row
+// the arithmetic is run_layer's: the attention walks each request's own
+// prefix rows then its suffix rows, the same key tiles in the same order as
+// the walk over all N rows whenever m is a multiple of the 64-key tile.
+// `first[g]` is group g's first request; segs are the deep layers' segments.
+bc_status run_last_layer(bc_model* mdl, int l, float* R, long full_rows, const Seg* segs, const int* first,
+                         int n_groups, int B, int n_s, float* out, char* ws, const Plan& p, hipStream_t s) {
+  const bc_model_config& c = mdl->cfg;
+  const bc_layer_weights& w = mdl->layers[l];
+  const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
+  const int hd = Hq * dh;
+  uint16_t* xn = (uint16_t*)(ws + p.xn);
+  uint16_t* q = (uint16_t*)(ws + p.q);
+  uint16_t* ao = (uint16_t*)(ws + p.ao);
+  void* act = ws + p.act;
+  const float* cos_t = (const float*)(ws + p.cos);
+  const float* sin_t = (const float*)(ws + p.sin);
+
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(R, w.attn_norm, xn, (int)full_rows, h, c.rms_eps, s));
+  for (int i = 0; i < n_groups; ++i) {
+    const Seg& g = segs[i];
+    const int N = g.n_seq, m = N - n_s;
+    uint16_t* qg = q + g.row0 * hd;
+    bc::QkvOut qo{qg, g.k_dst, g.v_dst, (long)Hq * N * dh, (long)N * dh,
+                  g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh, w.b_qkv};
+    BC_LAUNCH(mdl, BC_K_QKV, s,
+              bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, g.n_req * N, h, Hq, Hkv, dh, N, g.pos0,
+                                cos_t, sin_t, qo, s));
+    BC_LAUNCH(mdl, BC_K_OTHER, s,
+              bc::gather_suffix(R + g.row0 * h, out + (long)first[i] * n_s * h, g.n_req, m, n_s, h, s));
+    bc::AttnArgs a{};
+    a.q = qg + (long)m * dh;  // the suffix query rows of every (request, head)
+    a.q_sb = (long)Hq * N * dh;
+    a.q_sh = (long)N * dh;
+    a.q_sr = dh;
+    a.kp = g.k_dst;           // each request's own prefix rows 0..m-1
+    a.vp = g.v_dst;
+    a.p_sb = g.kv_sb;
+    a.p_sh = g.kv_sh;
+    a.ks = (const uint16_t*)g.k_dst + (long)m * dh;   // and its suffix rows m..N-1
+    a.vs = (const uint16_t*)g.v_dst + (long)m * dh;
+    a.s_sb = g.kv_sb;
+    a.s_sh = g.kv_sh;
+    a.s_sr = dh;
+    a.out = ao + (long)first[i] * n_s * hd;
+    a.o_sb = (long)n_s * hd;
+    a.o_sh = dh;
+    a.o_sr = hd;
+    a.B = g.n_req;
+    a.Hq = Hq;
+    a.Hkv = Hkv;
+    a.m = m;
+    a.n_s = n_s;
+    a.dh = dh;
+    a.scale = 1.f / sqrtf((float)dh);
+    a.out_f32 = 0;
+    BC_LAUNCH(mdl, BC_K_ATTN_FULL, s, bc::attention(a, s));
+  }
+  const int rows = B * n_s;
+  BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, out, h, s));
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(out, w.ffn_norm, xn, rows, h, c.rms_eps, s));
+  BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
+  BC_LAUNCH(mdl, BC_K_DOWN, s, bc::gemm_residual(act, F, w.w_down, F, rows, h, F, out, h, s));
+  return BC_OK;
+}
+
 bool step_shape_ok(const bc_model_config& c, int m, int B, int n_s, int d, std::string* why) {
   char buf[256];
   if (m < 1 || B < 1 || n_s < 1) {
@@ -490,6 +561,8 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
       row0 += (long)cnt * (m + n_s);
       first += cnt;
     }
+    std::vector<int> firsts(n_groups);
+    for (int g = 0, f = 0; g < n_groups; f += groups[g].count, ++g) firsts[g] = f;
     for (int l = d; l < L; ++l) {
       row0 = 0;
       for (int g = 0; g < n_groups; ++g) {
@@ -499,18 +572,15 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
         segs[g] = Seg{row0, cnt, N, 0, nullptr, nullptr, 0, kd, vd, kvd * N, (long)N * dh};
         row0 += (long)cnt * N;
       }
-      LayerCall lc{R, full_rows, segs.data(), n_groups};
-      bc_status st = run_layer(model, l, lc, ws, p, s);
+      bc_status st;
+      if (l + 1 < L) {
+        LayerCall lc{R, full_rows, segs.data(), n_groups};
+        st = run_layer(model, l, lc, ws, p, s);
+      } else {  // the last layer also moves the suffix rows of the residual to `out`
+        st = run_last_layer(model, l, R, full_rows, segs.data(), firsts.data(), n_groups, (int)B, n_s, out, ws,
+                            p, s);
+      }
       if (st != BC_OK) return st;
-    }
-    row0 = 0;
-    first = 0;
-    for (int g = 0; g < n_groups; ++g) {
-      const int m = ents[g]->m, cnt = groups[g].count;
-      BC_LAUNCH(model, BC_K_OTHER, s,
-                bc::gather_suffix(R + row0 * h, out + first * n_s * h, cnt, m, n_s, h, s));
-      row0 += (long)cnt * (m + n_s);
-      first += cnt;
     }
     if (use_store) {
       const DeepTag tg{key0, m0, (int)B, n_s, d, g_deep_nonce.fetch_add(1)};
