@@ -496,8 +496,11 @@ def time_populate(model, key, xp, Lc, cfg, torch, reps=3):
     t = sorted(ts)[len(ts) // 2]
     h, F, L = cfg["hidden"], cfg["ffn"], cfg["n_layers"]
     Hq, Hkv, dh = cfg["n_heads"], cfg["n_kv_heads"], cfg["head_dim"]
-    lin = 2 * (h * (Hq + 2 * Hkv) * dh + Hq * dh * h + 3 * h * F)
+    lin_qkv = 2 * h * (Hq + 2 * Hkv) * dh
+    lin = lin_qkv + 2 * (Hq * dh * h + 3 * h * F)
     flops = Lc * (m * lin + 4 * Hq * m * m * dh)
+    if Lc == L:   # the last layer's output residual has no H$ slot: only its K/V are computed
+        flops -= m * (lin - lin_qkv) + 4 * Hq * m * m * dh
     kv_bytes = Lc * 2 * Hkv * m * dh * 2
     h_bytes = min(Lc + 1, L) * m * h * 4
     return {"ms": round(t, 3), "tflops": round(flops / (t / 1e3) / 1e12, 1),

@@ -132,7 +132,9 @@ size_t bc_populate_workspace_bytes(const bc_model* model, int m);
 
 /* Populate on a miss (Sec. 5.2): runs the prefix-only forward x_pref = p at
  * positions 0..m-1 through layers 0..Lc-1, writes the entry into cache_mem
- * (layout above) and inserts `key` into the store.  If the store is full the
+ * (layout above) and inserts `key` into the store.  With Lc = L the residual
+ * after the last layer has no H$ slot, so that layer computes its K/V only
+ * (norm and Q/K/V projection).  If the store is full the
  * oldest entry is evicted first: *evicted = 1 and *evicted_key = its key (the
  * caller may free that entry's memory once `stream` has passed this call);
  * otherwise *evicted = 0, *evicted_key = 0 (either output may be NULL).

@@ -278,8 +278,10 @@ struct LayerCall {
   int n_segs;
 };
 
+// kv_only: only the layer's K/V are needed (a populate's last layer whose
+// output residual no cache slot keeps): norm and Q/K/V projection, nothing after.
 bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const Plan& p,
-                    hipStream_t s) {
+                    hipStream_t s, bool kv_only = false) {
   const bc_model_config& c = mdl->cfg;
   const bc_layer_weights& w = mdl->layers[l];
   const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
@@ -302,6 +304,7 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
     BC_LAUNCH(mdl, BC_K_QKV, s,
               bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, seg_rows, h, Hq, Hkv, dh, g.n_seq,
                                 g.pos0, cos_t, sin_t, qo, s));
+    if (kv_only) continue;
     bc::AttnArgs a{};
     a.q = qg;
     a.q_sb = (long)Hq * g.n_seq * dh;
@@ -330,6 +333,7 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
     a.out_f32 = 0;
     BC_LAUNCH(mdl, g.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
   }
+  if (kv_only) return BC_OK;
   BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, lc.R, h, s));
   BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.ffn_norm, xn, rows, h, c.rms_eps, s));
   BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
@@ -808,7 +812,9 @@ bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix
     char* v_dst = cm + (size_t)(2 * l + 1) * e.kv_layer;
     const Seg sg{0, 1, m, 0, nullptr, nullptr, 0, k_dst, v_dst, 0, (long)m * c.head_dim};
     LayerCall lc{R, m, &sg, 1};
-    bc_status st = run_layer(model, l, lc, ws, p, s);
+    // when no H$ slot keeps the residual this layer produces (Lc = L: the last
+    // layer), only its K/V are cached and nothing after Q/K/V is computed
+    bc_status st = run_layer(model, l, lc, ws, p, s, l + 1 >= e.n_h);
     if (st != BC_OK) return st;
   }
   bc::CacheEntry ce;
