@@ -271,22 +271,39 @@ struct Seg {
   long kp_sb = 0, kp_sh = 0;
 };
 
+// How much of a layer runs.  kAll: the whole layer over lc.rows rows.
+// kKvOnly: norm and Q/K/V projection only (a populate's last layer whose
+// output residual no cache slot keeps).  kSuffixOut: the last layer of a step
+// whose deep layers run over every row.  Only the suffix rows' outputs are
+// ever read there (the step returns them; nothing reads the prefix rows'
+// hidden states after the last layer), so once Q/K/V of every row are
+// projected (the suffix rows attend to the recomputed prefix K/V, Eq. 5 first
+// case) the suffix rows of the residual move to lc.out, and attention, the O
+// projection and the FFN run over those rows alone.  Per row the arithmetic
+// is that of kAll: the attention walks each request's own prefix rows then its
+// suffix rows, the same key tiles in the same order as the walk over all N
+// rows whenever m is a multiple of the 64-key tile.
+enum class LayerPart { kAll, kKvOnly, kSuffixOut };
+
 struct LayerCall {
   float* R;
   long rows;
   const Seg* segs;
   int n_segs;
+  // kSuffixOut: the suffix rows' residual [B][n_s][h]; segment i's requests
+  // start at request first[i]
+  float* out = nullptr;
+  const int* first = nullptr;
+  int B = 0, n_s = 0;
 };
 
-// kv_only: only the layer's K/V are needed (a populate's last layer whose
-// output residual no cache slot keeps): norm and Q/K/V projection, nothing after.
 bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const Plan& p,
-                    hipStream_t s, bool kv_only = false) {
+                    hipStream_t s, LayerPart part = LayerPart::kAll) {
   const bc_model_config& c = mdl->cfg;
   const bc_layer_weights& w = mdl->layers[l];
   const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
-  const int rows = (int)lc.rows;
   const int hd = Hq * dh;
+  const bool sfx = part == LayerPart::kSuffixOut;
   uint16_t* xn = (uint16_t*)(ws + p.xn);  // bf16 bits
   uint16_t* q = (uint16_t*)(ws + p.q);
   uint16_t* ao = (uint16_t*)(ws + p.ao);
@@ -294,121 +311,71 @@ bc_status run_layer(bc_model* mdl, int l, const LayerCall& lc, char* ws, const P
   const float* cos_t = (const float*)(ws + p.cos);
   const float* sin_t = (const float*)(ws + p.sin);
 
-  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.attn_norm, xn, rows, h, c.rms_eps, s));
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.attn_norm, xn, (int)lc.rows, h, c.rms_eps, s));
   for (int i = 0; i < lc.n_segs; ++i) {
     const Seg& g = lc.segs[i];
-    const int seg_rows = g.n_req * g.n_seq;
-    uint16_t* qg = q + g.row0 * hd;
-    bc::QkvOut qo{qg, g.k_dst, g.v_dst, (long)Hq * g.n_seq * dh, (long)g.n_seq * dh,
-                  g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh, w.b_qkv};
-    BC_LAUNCH(mdl, BC_K_QKV, s,
-              bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, seg_rows, h, Hq, Hkv, dh, g.n_seq,
-                                g.pos0, cos_t, sin_t, qo, s));
-    if (kv_only) continue;
-    bc::AttnArgs a{};
-    a.q = qg;
-    a.q_sb = (long)Hq * g.n_seq * dh;
-    a.q_sh = (long)g.n_seq * dh;
-    a.q_sr = dh;
-    a.kp = g.kp;
-    a.vp = g.vp;
-    a.p_sb = g.kp_sb;
-    a.p_sh = g.kp_sh ? g.kp_sh : (long)g.m_pre * dh;
-    a.ks = g.k_dst;
-    a.vs = g.v_dst;
-    a.s_sb = g.kv_sb;
-    a.s_sh = g.kv_sh;
-    a.s_sr = dh;
-    a.out = ao + g.row0 * hd;  // token-major [req, t, head, dim]: the O projection's A operand
-    a.o_sb = (long)g.n_seq * hd;
-    a.o_sh = dh;
-    a.o_sr = hd;
-    a.B = g.n_req;
-    a.Hq = Hq;
-    a.Hkv = Hkv;
-    a.m = g.m_pre;
-    a.n_s = g.n_seq;
-    a.dh = dh;
-    a.scale = 1.f / sqrtf((float)dh);
-    a.out_f32 = 0;
-    BC_LAUNCH(mdl, g.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
-  }
-  if (kv_only) return BC_OK;
-  BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, lc.R, h, s));
-  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(lc.R, w.ffn_norm, xn, rows, h, c.rms_eps, s));
-  BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
-  BC_LAUNCH(mdl, BC_K_DOWN, s, bc::gemm_residual(act, F, w.w_down, F, rows, h, F, lc.R, h, s));
-  return BC_OK;
-}
-
-// The last layer of a step whose deep layers run over every row.  Only the
-// suffix rows' outputs are ever read (the step returns them; nothing reads
-// the prefix rows' hidden states after the last layer), so once Q/K/V of
-// every row are projected (the suffix rows attend to the recomputed prefix
-// K/V, Eq. 5 first case) the suffix rows of the residual move to `out`, and
-// attention, the O projection and the FFN run over those rows alone.  Per row
-// the arithmetic is run_layer's: the attention walks each request's own
-// prefix rows then its suffix rows, the same key tiles in the same order as
-// the walk over all N rows whenever m is a multiple of the 64-key tile.
-// `first[g]` is group g's first request; segs are the deep layers' segments.
-bc_status run_last_layer(bc_model* mdl, int l, float* R, long full_rows, const Seg* segs, const int* first,
-                         int n_groups, int B, int n_s, float* out, char* ws, const Plan& p, hipStream_t s) {
-  const bc_model_config& c = mdl->cfg;
-  const bc_layer_weights& w = mdl->layers[l];
-  const int h = c.hidden, Hq = c.n_heads, Hkv = c.n_kv_heads, dh = c.head_dim, F = c.ffn;
-  const int hd = Hq * dh;
-  uint16_t* xn = (uint16_t*)(ws + p.xn);
-  uint16_t* q = (uint16_t*)(ws + p.q);
-  uint16_t* ao = (uint16_t*)(ws + p.ao);
-  void* act = ws + p.act;
-  const float* cos_t = (const float*)(ws + p.cos);
-  const float* sin_t = (const float*)(ws + p.sin);
-
-  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(R, w.attn_norm, xn, (int)full_rows, h, c.rms_eps, s));
-  for (int i = 0; i < n_groups; ++i) {
-    const Seg& g = segs[i];
-    const int N = g.n_seq, m = N - n_s;
+    const int N = g.n_seq;
     uint16_t* qg = q + g.row0 * hd;
     bc::QkvOut qo{qg, g.k_dst, g.v_dst, (long)Hq * N * dh, (long)N * dh,
                   g.kv_sb, g.kv_sh, g.kv_sb, g.kv_sh, w.b_qkv};
     BC_LAUNCH(mdl, BC_K_QKV, s,
               bc::gemm_qkv_rope(xn + g.row0 * h, h, w.w_qkv, h, g.n_req * N, h, Hq, Hkv, dh, N, g.pos0,
                                 cos_t, sin_t, qo, s));
-    BC_LAUNCH(mdl, BC_K_OTHER, s,
-              bc::gather_suffix(R + g.row0 * h, out + (long)first[i] * n_s * h, g.n_req, m, n_s, h, s));
+    if (part == LayerPart::kKvOnly) continue;
     bc::AttnArgs a{};
-    a.q = qg + (long)m * dh;  // the suffix query rows of every (request, head)
     a.q_sb = (long)Hq * N * dh;
     a.q_sh = (long)N * dh;
     a.q_sr = dh;
-    a.kp = g.k_dst;           // each request's own prefix rows 0..m-1
-    a.vp = g.v_dst;
-    a.p_sb = g.kv_sb;
-    a.p_sh = g.kv_sh;
-    a.ks = (const uint16_t*)g.k_dst + (long)m * dh;   // and its suffix rows m..N-1
-    a.vs = (const uint16_t*)g.v_dst + (long)m * dh;
     a.s_sb = g.kv_sb;
     a.s_sh = g.kv_sh;
     a.s_sr = dh;
-    a.out = ao + (long)first[i] * n_s * hd;
-    a.o_sb = (long)n_s * hd;
-    a.o_sh = dh;
+    a.o_sh = dh;  // token-major [req, t, head, dim]: the O projection's A operand
     a.o_sr = hd;
     a.B = g.n_req;
     a.Hq = Hq;
     a.Hkv = Hkv;
-    a.m = m;
-    a.n_s = n_s;
     a.dh = dh;
     a.scale = 1.f / sqrtf((float)dh);
     a.out_f32 = 0;
-    BC_LAUNCH(mdl, BC_K_ATTN_FULL, s, bc::attention(a, s));
+    if (sfx) {
+      const int m = N - lc.n_s;
+      BC_LAUNCH(mdl, BC_K_OTHER, s,
+                bc::gather_suffix(lc.R + g.row0 * h, lc.out + (long)lc.first[i] * lc.n_s * h, g.n_req, m,
+                                  lc.n_s, h, s));
+      a.q = qg + (long)m * dh;  // the suffix query rows of every (request, head)
+      a.kp = g.k_dst;           // each request's own prefix rows 0..m-1
+      a.vp = g.v_dst;
+      a.p_sb = g.kv_sb;
+      a.p_sh = g.kv_sh;
+      a.ks = (const uint16_t*)g.k_dst + (long)m * dh;   // and its suffix rows m..N-1
+      a.vs = (const uint16_t*)g.v_dst + (long)m * dh;
+      a.out = ao + (long)lc.first[i] * lc.n_s * hd;
+      a.o_sb = (long)lc.n_s * hd;
+      a.m = m;
+      a.n_s = lc.n_s;
+      BC_LAUNCH(mdl, BC_K_ATTN_FULL, s, bc::attention(a, s));
+    } else {
+      a.q = qg;
+      a.kp = g.kp;
+      a.vp = g.vp;
+      a.p_sb = g.kp_sb;
+      a.p_sh = g.kp_sh ? g.kp_sh : (long)g.m_pre * dh;
+      a.ks = g.k_dst;
+      a.vs = g.v_dst;
+      a.out = ao + g.row0 * hd;
+      a.o_sb = (long)N * hd;
+      a.m = g.m_pre;
+      a.n_s = N;
+      BC_LAUNCH(mdl, g.m_pre > 0 ? BC_K_ATTN_SHARED : BC_K_ATTN_FULL, s, bc::attention(a, s));
+    }
   }
-  const int rows = B * n_s;
-  BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, out, h, s));
-  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(out, w.ffn_norm, xn, rows, h, c.rms_eps, s));
+  if (part == LayerPart::kKvOnly) return BC_OK;
+  float* R = sfx ? lc.out : lc.R;
+  const int rows = sfx ? lc.B * lc.n_s : (int)lc.rows;
+  BC_LAUNCH(mdl, BC_K_OPROJ, s, bc::gemm_residual(ao, hd, w.w_o, hd, rows, h, hd, R, h, s));
+  BC_LAUNCH(mdl, BC_K_RMSNORM, s, bc::rmsnorm(R, w.ffn_norm, xn, rows, h, c.rms_eps, s));
   BC_LAUNCH(mdl, BC_K_GATE_UP, s, bc::gemm_swiglu(xn, h, w.w_gate_up, h, rows, F, h, act, s));
-  BC_LAUNCH(mdl, BC_K_DOWN, s, bc::gemm_residual(act, F, w.w_down, F, rows, h, F, out, h, s));
+  BC_LAUNCH(mdl, BC_K_DOWN, s, bc::gemm_residual(act, F, w.w_down, F, rows, h, F, R, h, s));
   return BC_OK;
 }
 
@@ -576,14 +543,9 @@ bc_status step_impl(bc_model* model, const Group* groups, int n_groups, const vo
         segs[g] = Seg{row0, cnt, N, 0, nullptr, nullptr, 0, kd, vd, kvd * N, (long)N * dh};
         row0 += (long)cnt * N;
       }
-      bc_status st;
-      if (l + 1 < L) {
-        LayerCall lc{R, full_rows, segs.data(), n_groups};
-        st = run_layer(model, l, lc, ws, p, s);
-      } else {  // the last layer also moves the suffix rows of the residual to `out`
-        st = run_last_layer(model, l, R, full_rows, segs.data(), firsts.data(), n_groups, (int)B, n_s, out, ws,
-                            p, s);
-      }
+      // the last layer also moves the suffix rows of the residual to `out`
+      const LayerCall lc{R, full_rows, segs.data(), n_groups, out, firsts.data(), (int)B, n_s};
+      bc_status st = run_layer(model, l, lc, ws, p, s, l + 1 < L ? LayerPart::kAll : LayerPart::kSuffixOut);
       if (st != BC_OK) return st;
     }
     if (use_store) {
@@ -814,7 +776,7 @@ bc_status bc_prefix_populate(bc_model* model, uint64_t key, const void* x_prefix
     LayerCall lc{R, m, &sg, 1};
     // when no H$ slot keeps the residual this layer produces (Lc = L: the last
     // layer), only its K/V are cached and nothing after Q/K/V is computed
-    bc_status st = run_layer(model, l, lc, ws, p, s, l + 1 >= e.n_h);
+    bc_status st = run_layer(model, l, lc, ws, p, s, l + 1 >= e.n_h ? LayerPart::kKvOnly : LayerPart::kAll);
     if (st != BC_OK) return st;
   }
   bc::CacheEntry ce;
