@@ -97,7 +97,7 @@ def main():
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
         print(f"bench.py measures the single-GPU path only (asked for --gpus {args.gpus}, "
-              f"WORLD_SIZE={world}); multi-GPU sharding is described in DESIGN.md, not run.",
+              f"WORLD_SIZE={world}); the step shards by request across GPUs, which is not implemented here.",
               file=sys.stderr)
         sys.exit(2)
 

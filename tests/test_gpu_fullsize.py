@@ -66,7 +66,7 @@ def test_c4_populate_every_layer():
     """The C4 populate (m 8192, the first 8 layers of the C3 shape) against the
     oracle's prefix-only forward (Sec. 5.2 miss path): K and V of every cached
     layer, head and position (bf16 storage bound), every cached residual H$[l]
-    (fp32, the benchmark spec's tolerance), H$[0] bit-exact."""
+    (fp32, max-abs 2e-2 / mean-abs 2e-3), H$[0] bit-exact."""
     cfg = synth.model_config(n_layers=8)
     m = synth.POPULATE_C4["m"]
     h, Hkv, dh = cfg["hidden"], cfg["n_kv_heads"], cfg["head_dim"]
