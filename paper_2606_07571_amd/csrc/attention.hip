@@ -41,16 +41,23 @@
 // Software pipeline.  Every wave overlaps its own matrix and vector work: in
 // step u it runs
 //   block A: O^T += V(u-1)^T . P(u-1)^T (16 MFMAs) alongside the softmax of
-//            S(u) (row max, running max, P(u) = exp2(...), row sums)
+//            S(u) (P(u) = exp2(...) against the running max, row sums)
 //   block B: S(u+1)^T = K(u+1) . Q^T (16 MFMAs) alongside this thread's share
 //            of the LDS fill of tile u+2 and the global fetch of tile u+4
 // and one barrier.  The MFMAs of a block do not depend on its vector work, so
 // the two streams issue side by side, and with two such waves per SIMD the
 // vector instructions issue at the SIMD's full rate (one wave alone issues
-// one only every other slot).  The online softmax stays exact: the running
-// max moves (lazily, by more than 8 in log2 units) before P(u) is formed, and
-// O, which holds P(u-1).V(u-1) computed with the old max once block A is
-// done, is rescaled between the blocks.
+// one only every other slot).  The online softmax stays exact with a running
+// max that moves rarely: the first tile sets it to the tile's row max; after
+// that P(u) is formed against it directly and the tile's row sums, which come
+// from the matrix pipe anyway, bound every probability.  Only a sum above
+// 2^16 (a score far above the running max, or a row that had no valid key
+// yet) moves the max to the tile's and forms P(u) again; O, which holds
+// P(u-1).V(u-1) computed with the old max once block A is done, is then
+// rescaled between the blocks.  Any running max gives the same result up to
+// the bf16 rounding of P, since O and the row sum carry the same factor; the
+// bound keeps probabilities, and so O and the row sums, far from overflow.
+// No row max is taken on the common path.
 //
 // LDS.  Tiles live in a 4-deep ring (tile t in slot t % 4): step u reads
 // V(u-1) and K(u+1) and fills tile u+2, whose slot last held tile u-2.  The
@@ -309,12 +316,12 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     const u32x4 pv4 = {pw[0], pw[1], pw[2], pw[3]};
     return __builtin_bit_cast(bf16x8, pv4);
   };
-  // The running max moves only when some row's tile max exceeds it by more
-  // than 8 (log2 units), so probabilities stay <= 2^8; returns the factor
+  // Row max of the first tile (step 0): the running max moves when some
+  // row's tile max exceeds it by more than 8 (log2 units); returns the factor
   // that moves O and the row sum to the new max (1 when it does not move).
-  // The first tile of a row always moves it (m starts at -inf, kept finite
-  // so that fully masked tiles give exp2(-inf) = 0).
-  bool moved = false;   // wave-uniform: the last new_max moved the running max
+  // m starts at -inf, kept finite so that fully masked tiles give
+  // exp2(-inf) = 0 and leave it there.
+  bool moved = false;   // wave-uniform: the running max moved in this step
   auto new_max = [&](const f32x16 (&sc)[2]) __attribute__((always_inline)) {
     float mx = -INFINITY;
 #pragma unroll
@@ -337,9 +344,10 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
   // MFMAs interleaved with its share of the vector work, so fragment reads
   // have a whole sub-block to arrive and a wave never waits on LDS with
   // independent work queued behind the wait.
-  //   P.V sub-block s:   softmax of S(u): the row max and running max (s = 0)
-  //                      and P(u)'s k step s, written into the registers the
-  //                      sub-block's MFMAs have just read
+  //   P.V sub-block s:   softmax of S(u): P(u)'s k step s, written into the
+  //                      registers the sub-block's MFMAs have just read, and
+  //                      its row sums; after the last, the bound check (and,
+  //                      rarely, the max move and P(u) again)
   //   QK sub-blocks:     LDS fill of tile u+2, fetch of tile u+3
   // p holds P(u-1) on entry and P(u) on exit; sc holds S(u) on entry and
   // S(u+1) on exit; fr[0] holds the first sub-block's fragments on entry and
@@ -382,7 +390,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
 #pragma unroll
           for (int nb = 0; nb < NB; ++nb) o[nb] = mfma_32x32x16(fr[j & 1][nb], p[j], o[nb]);
         }
-        if (j == 0) alpha = new_max(sc);
+        if (!PV && j == 0) alpha = new_max(sc);
         p[j] = probs(sc, j);
         // pin P(u)'s step j here: otherwise the compiler defers the softmax
         // past the QK MFMAs and keeps a second copy of S(u) alive
@@ -410,6 +418,28 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       }
       __builtin_amdgcn_sched_barrier(0);
       if (j == NS - 1) {
+        if constexpr (PV) {
+          // a row sum above 2^16 (or not finite) means a probability may be:
+          // move the max to the tile's and form P(u) and its sums again
+          const bool big = __builtin_amdgcn_ballot_w64(!(ltile[0] <= 65536.f && ltile[1] <= 65536.f)) != 0;
+          moved = big;
+          if (big) {
+            float mx = -INFINITY;
+#pragma unroll
+            for (int kb = 0; kb < 2; ++kb)
+#pragma unroll
+              for (int e = 0; e < 16; ++e) mx = fmaxf(mx, sc[kb][e]);
+            const float m_new = fmaxf(m_run, half_max(mx) * sl2);
+            alpha = __builtin_amdgcn_exp2f(m_run - m_new);
+            m_run = m_new;
+            ltile = f32x4{0.f, 0.f, 0.f, 0.f};
+#pragma unroll
+            for (int s = 0; s < NS; ++s) {
+              p[s] = probs(sc, s);
+              ltile = __builtin_amdgcn_mfma_f32_16x16x32_bf16(ones_sel, p[s], ltile, 0, 0, 0);
+            }
+          }
+        }
         if (moved) {
           // rare: the running max moved; O already holds P(u-1).V(u-1)
 #pragma unroll
