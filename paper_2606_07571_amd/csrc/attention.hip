@@ -183,7 +183,14 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       }
     }
   };
-  enter(0, b_lo);
+  // -1 when the keys of the segment at the cursor are this wave's (the shared
+  // prefix, or its own request's), else 0: set once per segment
+  int w_mask = 0;
+  auto enter_seg = [&](int phase, int req) __attribute__((always_inline)) {
+    enter(phase, req);
+    w_mask = (active && (w_req < 0 || w_req == b)) ? -1 : 0;
+  };
+  enter_seg(0, b_lo);
   // valid keys of each fetched tile for this wave (0 for tiles of another
   // request and past the end), queued from fetch to use: tiles u..u+3
   int nvq0 = 0, nvq1 = 0, nvq2 = 0, nvq3 = 0, nvq4 = 0;
@@ -211,7 +218,7 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
     constexpr int S = decltype(set_c)::value;
     const int nv = min(KT, w_left);
     const int bytes = nv * DH * 2;
-    nvq4 = (active && (w_req < 0 || w_req == b)) ? nv : 0;
+    nvq4 = nv & w_mask;
     const auto rk = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wk), (short)0, bytes, RSRC_W3);
     const auto rv = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16*>(wv), (short)0, bytes, RSRC_W3);
     if (w_left > KT) {
@@ -219,9 +226,9 @@ __global__ void __launch_bounds__(512) attn_il_kernel(AttnArgs a, int CQ, int wg
       wv += KT * DH;
       w_left -= KT;
     } else if (w_req <= b_hi) {
-      if (w_phase == 0) enter(own_pre ? 1 : 2, b_lo);
-      else if (w_phase == 1) enter(2, w_req);
-      else enter(own_pre ? 1 : 2, w_req + 1);
+      if (w_phase == 0) enter_seg(own_pre ? 1 : 2, b_lo);
+      else if (w_phase == 1) enter_seg(2, w_req);
+      else enter_seg(own_pre ? 1 : 2, w_req + 1);
     }
 #pragma unroll
     for (int p = 0; p < K_PER; ++p) kreg[S][p] = __builtin_amdgcn_raw_buffer_load_b128(rk, kg_off[p], 0, 0);
