@@ -442,26 +442,28 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
 
   // fragment f < 4: A block f, f >= 4: W block f - 4, of substep s of K step k
   bf16x8 fr[2][8];
-  auto read_frag = [&](int k, int s, int set, int f) __attribute__((always_inline)) {
+  // a3 = k % 3 and b2 = k % 2: the ring slots of K step k's A and W tiles
+  auto read_frag = [&](int a3, int b2, int s, int set, int f) __attribute__((always_inline)) {
     const int kci = s * 2 + (lane >> 5);
     if (f < 4)
-      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sA[k % 3][swz(wm * TM + f * 32 + (lane & 31), kci)]);
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sA[a3][swz(wm * TM + f * 32 + (lane & 31), kci)]);
     else
-      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sB[k & 1][swz(wn * TN + (f - 4) * 32 + (lane & 31), kci)]);
+      fr[set][f] = *reinterpret_cast<const bf16x8*>(&sB[b2][swz(wn * TN + (f - 4) * 32 + (lane & 31), kci)]);
   };
   // reads in the order the next phase's MFMAs need them
   constexpr int kReadOrder[8] = {0, 4, 5, 6, 7, 1, 2, 3};
   // One phase: the 16 MFMAs of the fragments in set mset (if MMA), the 8
-  // fragment reads of substep rs of K step rk into set rset (if RD), and (if
-  // LD) 4 loads q0 .. q0+3 of the K step at k0 into buffer dbuf, one per 4 MFMAs.
-  auto phase = [&](auto MMA, auto RD, auto LD, int mset, int rk, int rs, int rset, int q0, int dbuf, int k0)
+  // fragment reads of substep rs of the K step in slots (a3, b2) into set rset
+  // (if RD), and (if LD) 4 loads q0 .. q0+3 of the K step at k0 into buffer
+  // dbuf, one per 4 MFMAs.
+  auto phase = [&](auto MMA, auto RD, auto LD, int mset, int a3, int b2, int rs, int rset, int q0, int dbuf, int k0)
       __attribute__((always_inline)) {
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       if constexpr (decltype(MMA)::value)
         acc[q >> 2][q & 3] = mfma_32x32x16(fr[mset][q >> 2], fr[mset][4 + (q & 3)], acc[q >> 2][q & 3]);
       if constexpr (decltype(RD)::value)
-        if ((q & 1) == 0) read_frag(rk, rs, rset, kReadOrder[q >> 1]);
+        if ((q & 1) == 0) read_frag(a3, b2, rs, rset, kReadOrder[q >> 1]);
       if constexpr (decltype(LD)::value)
         if ((q & 3) == 0) load(q0 + (q >> 2), dbuf, k0);
       __builtin_amdgcn_sched_barrier(0);
@@ -488,33 +490,45 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
   } else {
     wait_loads_barrier();
   }
-  auto body = [&](int k, auto FIRST, auto LDW, auto LDA) __attribute__((always_inline)) {
+  // K step k, its ring slots a3 = k % 3, b2 = k % 2
+  auto body = [&](int k, auto FIRST, auto LDW, auto LDA, int a3, int b2) __attribute__((always_inline)) {
     const int k1 = (k + 1) * BK, k2 = (k + 2) * BK;
-    phase(std::integral_constant<bool, !decltype(FIRST)::value>{}, T{}, LDW, 1, k, 0, 0, 8, (k + 1) & 1, k1);
-    phase(T{}, T{}, LDW, 0, k, 1, 1, 12, (k + 1) & 1, k1);
-    phase(T{}, T{}, LDA, 1, k, 2, 0, 0, (k + 2) % 3, k2);
-    phase(T{}, T{}, LDA, 0, k, 3, 1, 4, (k + 2) % 3, k2);
+    const int wb = 1 - b2, ab = a3 == 0 ? 2 : a3 - 1;   // (k + 1) % 2, (k + 2) % 3
+    phase(std::integral_constant<bool, !decltype(FIRST)::value>{}, T{}, LDW, 1, a3, b2, 0, 0, 8, wb, k1);
+    phase(T{}, T{}, LDW, 0, a3, b2, 1, 1, 12, wb, k1);
+    phase(T{}, T{}, LDA, 1, a3, b2, 2, 0, 0, ab, k2);
+    phase(T{}, T{}, LDA, 0, a3, b2, 3, 1, 4, ab, k2);
   };
   using B1 = std::true_type;
   using B0 = std::false_type;
   if (ksteps >= 3) {
-    body(0, B1{}, T{}, T{});
+    body(0, B1{}, T{}, T{}, 0, 0);
     wait_loads_but8_barrier();
-    for (int k = 1; k + 2 < ksteps; ++k) {
-      body(k, B0{}, T{}, T{});
-      wait_loads_but8_barrier();
+    // K steps 1 .. ksteps-3, six per pass (the ring periods are 3 and 2), so
+    // every LDS address of a step is a constant offset from a lane base: the
+    // slot arithmetic (k % 3 by multiplication) had cost about 20 scalar
+    // instructions at the head of every step, where they delay its second MFMA
+    int k = 1;
+    for (;;) {
+#define BC_KSTEP(A3, B2)                \
+      if (k + 2 >= ksteps) break;       \
+      body(k, B0{}, T{}, T{}, A3, B2);  \
+      wait_loads_but8_barrier();        \
+      ++k;
+      BC_KSTEP(1, 1) BC_KSTEP(2, 0) BC_KSTEP(0, 1) BC_KSTEP(1, 0) BC_KSTEP(2, 1) BC_KSTEP(0, 0)
+#undef BC_KSTEP
     }
-    body(ksteps - 2, B0{}, T{}, F{});
+    body(ksteps - 2, B0{}, T{}, F{}, (ksteps - 2) % 3, (ksteps - 2) & 1);
     wait_loads_barrier();
-    body(ksteps - 1, B0{}, F{}, F{});
+    body(ksteps - 1, B0{}, F{}, F{}, (ksteps - 1) % 3, (ksteps - 1) & 1);
   } else if (ksteps == 2) {
-    body(0, B1{}, T{}, F{});
+    body(0, B1{}, T{}, F{}, 0, 0);
     wait_loads_barrier();
-    body(1, B0{}, F{}, F{});
+    body(1, B0{}, F{}, F{}, 1, 1);
   } else {
-    body(0, B1{}, F{}, F{});
+    body(0, B1{}, F{}, F{}, 0, 0);
   }
-  phase(T{}, F{}, F{}, 1, 0, 0, 0, 0, 0, 0);
+  phase(T{}, F{}, F{}, 1, 0, 0, 0, 0, 0, 0, 0);
 
   // every wave is past its last LDS read: the tile buffers become the
   // epilogue's staging area, 64 KiB (of the A ring, or the W ring) per pair of
