@@ -454,16 +454,20 @@ __global__ void __launch_bounds__(256) gemm_kernel(GemmArgs a, Epi epi) {
   constexpr int kReadOrder[8] = {0, 4, 5, 6, 7, 1, 2, 3};
   // One phase: the 16 MFMAs of the fragments in set mset (if MMA), the 8
   // fragment reads of substep rs of the K step in slots (a3, b2) into set rset
-  // (if RD), and (if LD) 4 loads q0 .. q0+3 of the K step at k0 into buffer
-  // dbuf, one per 4 MFMAs.
+  // (if RD), one beside each of the first 8 MFMAs, and (if LD) 4 loads
+  // q0 .. q0+3 of the K step at k0 into buffer dbuf, one per 4 MFMAs.  The
+  // reads land during the phase's second half, so one wait at the head of the
+  // next phase covers all of them (and the wait before the step's closing
+  // barrier finds them done).
   auto phase = [&](auto MMA, auto RD, auto LD, int mset, int a3, int b2, int rs, int rset, int q0, int dbuf, int k0)
       __attribute__((always_inline)) {
+    if constexpr (decltype(MMA)::value) __builtin_amdgcn_s_waitcnt(0xC07F);   // lgkmcnt(0)
 #pragma unroll
     for (int q = 0; q < 16; ++q) {
       if constexpr (decltype(MMA)::value)
         acc[q >> 2][q & 3] = mfma_32x32x16(fr[mset][q >> 2], fr[mset][4 + (q & 3)], acc[q >> 2][q & 3]);
       if constexpr (decltype(RD)::value)
-        if ((q & 1) == 0) read_frag(a3, b2, rs, rset, kReadOrder[q >> 1]);
+        if (q < 8) read_frag(a3, b2, rs, rset, kReadOrder[q]);
       if constexpr (decltype(LD)::value)
         if ((q & 3) == 0) load(q0 + (q >> 2), dbuf, k0);
       __builtin_amdgcn_sched_barrier(0);
