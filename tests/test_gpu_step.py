@@ -27,6 +27,11 @@ SMALL = [
     # K = 192 (three: down); output tiles mostly empty (N = 64, 192)
     dict(cfg=synth.model_config(n_layers=2, hidden=64, n_heads=1, n_kv_heads=1, head_dim=64, ffn=192),
          m=77, n_s=33, B=3, seed=14),
+    # K loops of 5 and 7 steps (K = 320: QKV, O, gate/up; K = 448: down), which leave the
+    # GEMM's six-step unrolled loop after its second and fourth step; F = 448 is not a
+    # whole number of 128-column SwiGLU tiles
+    dict(cfg=synth.model_config(n_layers=2, hidden=320, n_heads=5, n_kv_heads=1, head_dim=64, ffn=448),
+         m=90, n_s=40, B=2, seed=15),
 ]
 
 
@@ -47,7 +52,7 @@ class Setup:
         self.cache64 = OT.populate(to_f64(self.xp), self.w64, cfg, cfg["n_layers"])
 
 
-@pytest.fixture(scope="module", params=range(len(SMALL)), ids=["gqa64", "mha128", "g7n1", "k64"])
+@pytest.fixture(scope="module", params=range(len(SMALL)), ids=["gqa64", "mha128", "g7n1", "k64", "k320"])
 def setup(request):
     s = Setup(SMALL[request.param])
     yield s
