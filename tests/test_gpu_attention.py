@@ -52,13 +52,14 @@ def test_ragged_and_gqa(shape):
     assert_close(got, ref, f"ragged {shape}")
 
 
+@pytest.mark.parametrize("dh", [128, 64])
 @pytest.mark.parametrize("order", ["rising", "falling"])
-def test_running_max_moves(order):
+def test_running_max_moves(order, dh):
     """Key rows scaled by a factor that grows (or shrinks) with their 64-key tile, so each
     tile's scores sit tens of log2 units above (or below) the last: the running max must
     move on most tiles (the rows' probability sums against the old max overflow the
     bound) and the tile's probabilities be formed again; falling scores underflow."""
-    shape = AttnShape(B=2, Hq=4, Hkv=2, m=320, n_s=96, dh=128)
+    shape = AttnShape(B=2, Hq=4, Hkv=2, m=320, n_s=96, dh=dh)
     say(f"attention case running max {order} {shape}")
     q, kp, vp, ks, vs = synth.attention_inputs(shape, 11, 1.0)
     f = 1.0 + 1.5 * (np.arange(shape.m + shape.n_s) // 64)
@@ -75,7 +76,7 @@ def test_running_max_moves(order):
     shared_prefix_attention(*[t.cuda() for t in cpu], scale=scale, out=out)
     torch.cuda.synchronize()
     ref = oracle_spa(*[to_f64(t) for t in cpu], scale)
-    assert_close(out.cpu().double().numpy(), ref, f"running max {order}")
+    assert_close(out.cpu().double().numpy(), ref, f"running max {order} dh={dh}")
 
 
 def test_constant_values_give_constant():
